@@ -1,0 +1,177 @@
+/*
+ * kbest.h -- C ABI of the MI355X (gfx950) output-layer library.
+ *
+ * One beam-search decode step of a neural MT output layer, as described in
+ * Hoang et al., "Fast Neural Machine Translation Implementation" (WNMT 2018):
+ *
+ *   Section 2.2, steps 1-4:  p = w x  ->  p = p + b  ->  softmax  ->  k-best;
+ *   Algorithm 4:             bias, softmax statistics and best-class search
+ *                            fused into one pass over the scores;
+ *   Algorithm 6:             the vocabulary is sharded, each shard reduced in
+ *                            parallel, then the shard results are merged;
+ *   Section 2.1, Alg. 2:     finished hypotheses are removed from the batch
+ *                            after every step (mini-batching).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every buffer argument is device memory owned by the caller (hipMalloc'd
+ *    or a framework tensor on the current device).  The library never
+ *    allocates, frees or synchronises, and keeps no mutable global state;
+ *    only the text returned by kb_last_error() is per thread.
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream).
+ *    Inputs must stay alive, and outputs must not be read, until the caller
+ *    has synchronised with that stream.
+ *  - Every function returns a kb_status and never aborts.  On any error the
+ *    outputs are unspecified and nothing has been enqueued, except for
+ *    KB_ERR_HIP, which reports a failed launch.
+ *  - Inputs must be finite.  Non-finite inputs give unspecified results but
+ *    no fault.
+ */
+#ifndef KBEST_H
+#define KBEST_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KB_ABI_VERSION 1
+#define KB_MAX_K 16 /* largest k (beam width of the output) supported */
+
+typedef enum kb_status {
+  KB_OK = 0,
+  KB_ERR_INVALID_ARG = 1, /* null pointer, bad size, k out of range, ... */
+  KB_ERR_UNSUPPORTED = 2, /* a valid request this build does not handle  */
+  KB_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required  */
+  KB_ERR_HIP = 4          /* a HIP launch failed; see kb_last_error()     */
+} kb_status;
+
+/* Storage type of h and W.  Bias, scores and all accumulation are float32. */
+typedef enum kb_dtype {
+  KB_F32 = 0,  /* float32 h and W; float32 products on the matrix cores      */
+  KB_BF16 = 1  /* bfloat16 h and W (the half-precision GEMM of Section 2.3);  */
+               /* exact bf16 x bf16 products, float32 accumulation           */
+} kb_dtype;
+
+/* KB_ABI_VERSION of the loaded library. */
+int kb_abi_version(void);
+
+/* Static text for a kb_status value. */
+const char* kb_status_string(int status);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char* kb_last_error(void);
+
+/*
+ * Workspace bytes kb_kbest_step needs for this shape (0 when N == 0).
+ * Depends only on (dtype, N, H, V, k, S); the same shape always gives the
+ * same size.
+ */
+size_t kb_kbest_workspace_bytes(int dtype, int N, int H, int V, int k, int S);
+
+/*
+ * kb_kbest_step -- one decode step of the output layer with the beam k-best.
+ *
+ * Computes, for every live hypothesis row n (Section 2.2 steps 1-3):
+ *     x[n, j]   = sum_i h[n, i] * W[i, j] + b[j]            (j < V)
+ *     LSE[n]    = log sum_j exp(x[n, j])
+ *     cand(n,j) = prev_score[n] + x[n, j] - LSE[n]         (cumulative log-prob)
+ * and, for every sentence s owning rows sent_offsets[s] .. sent_offsets[s+1]-1,
+ * the k best candidates over all of its rows and all words (step 4, extended
+ * from the 1-best scan of Algorithms 3-5 to k-best across the beam), sorted
+ * by descending score; equal scores keep the lower flat index
+ * (row - sent_offsets[s]) * V + j, i.e. the lower parent row, then the lower
+ * word -- the first-index-wins rule of the paper's strict '>' scans.
+ *
+ * The N x V scores are never written to memory: the projection's epilogue
+ * keeps, per row and vocabulary shard, the softmax statistics (Algorithm 4's
+ * running max and rescaled sum) and the k best (score, word) pairs, which a
+ * second kernel merges across shards (Algorithm 6) and across each
+ * sentence's rows.
+ *
+ * Arguments
+ *   dtype         KB_F32 or KB_BF16: element type of h and W.
+ *   N, H, V       rows (live hypotheses), state size, vocabulary size.
+ *                 N >= S, H >= 1, V >= 1.  N == S == 0 is a no-op.
+ *   k             outputs per sentence, 1 <= k <= min(KB_MAX_K, V).
+ *   S             sentences (beams) in the batch.
+ *   h             N x H row-major (H contiguous), element type `dtype`.
+ *   W             H x V row-major (V contiguous), element type `dtype`.
+ *   b             V float32 bias.
+ *   prev_score    N float32 cumulative log-probability of each row.
+ *   sent_offsets  S+1 int32 (the beam map): 0 = off[0] < off[1] < ... <
+ *                 off[S] = N; every sentence owns at least one row.  Device
+ *                 contents are trusted (not checked).
+ *   out_token     S x k int32: word index in [0, V).
+ *   out_parent    S x k int32: global row index of the parent hypothesis.
+ *   out_score     S x k float32: cumulative log-probability, descending.
+ *   out_row_lse   nullable; N float32 log-sum-exp of each row.
+ *   workspace     device scratch of at least kb_kbest_workspace_bytes(...)
+ *                 bytes, 256-byte aligned; contents need no initialisation
+ *                 and are overwritten.
+ *   stream        hipStream_t.
+ * h and W must be aligned to their element size; 16-byte alignment with H
+ * and V multiples of 8 (bf16) or 4 (f32) enables vector loads.
+ */
+int kb_kbest_step(int dtype, int N, int H, int V, int k, int S,
+                  const void* h, const void* W, const float* b,
+                  const float* prev_score, const int32_t* sent_offsets,
+                  int32_t* out_token, int32_t* out_parent, float* out_score,
+                  float* out_row_lse,
+                  void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * kb_kbest_step_events -- kb_kbest_step that also records two HIP events
+ * (hipEvent_t, both nullable) on `stream` immediately before and after the
+ * fused projection kernel, so a caller can time that kernel alone.
+ */
+int kb_kbest_step_events(int dtype, int N, int H, int V, int k, int S,
+                         const void* h, const void* W, const float* b,
+                         const float* prev_score, const int32_t* sent_offsets,
+                         int32_t* out_token, int32_t* out_parent, float* out_score,
+                         float* out_row_lse,
+                         void* workspace, size_t workspace_bytes, void* stream,
+                         void* proj_begin_event, void* proj_end_event);
+
+/*
+ * kb_compact_batch -- remove finished hypotheses from the batch (Section 2.1,
+ * Algorithm 2: after each Decode, every hypothesis that produced EOS leaves
+ * the batch; decoding stops when the batch is empty).
+ *
+ * The batch is the S x k output of kb_kbest_step, sentence-major: entry
+ * i = s*k + r is the r-th continuation of sentence s.
+ *   alive             S*k uint8, nonzero = the entry stays in the batch.
+ *   keep_idx          S*k int32; the first *kept_count entries receive the
+ *                     indices of the surviving entries in ascending order
+ *                     (a stable compaction); the rest is left untouched.
+ *   kept_count        device int32 scalar: number of surviving entries.
+ *   new_sent_offsets  nullable, S+1 int32: the first *new_S + 1 entries are
+ *                     the row offsets of the compacted batch (sentences with
+ *                     no surviving entry are dropped).
+ *   kept_sentence     nullable, S int32: for each surviving sentence, its
+ *                     index in the old batch.
+ *   new_S             nullable, device int32 scalar: surviving sentences.
+ * S == 0 writes kept_count = 0 (and new_S = 0, new_sent_offsets[0] = 0).
+ * 1 <= k; S*k must fit in int32.  Results are exact (integer work).
+ */
+int kb_compact_batch(int S, int k, const uint8_t* alive, int32_t* keep_idx,
+                     int32_t* kept_count, int32_t* new_sent_offsets,
+                     int32_t* kept_sentence, int32_t* new_S, void* stream);
+
+/*
+ * kb_gather_rows -- dst[i, :] = src[idx[i], :] for i < n, where
+ * n = min(n_max, *n_dev) if n_dev is non-null, else n_max.  Rows are
+ * row_bytes long (a multiple of 4); src, dst 4-byte aligned.  Moves the
+ * per-hypothesis state of the surviving entries after kb_compact_batch.
+ * idx values must index valid rows of src (not checked).
+ */
+int kb_gather_rows(int n_max, const int32_t* n_dev, const int32_t* idx,
+                   const void* src, void* dst, size_t row_bytes, void* stream);
+
+#ifdef __cplusplus
+} /* extern "C" */
+#endif
+
+#endif /* KBEST_H */

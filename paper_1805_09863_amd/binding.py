@@ -1,0 +1,197 @@
+"""ctypes binding of libkbest (the C ABI in include/kbest.h).
+
+Argument marshalling only: every step of the output layer runs in the HIP
+kernels of libkbest.  PyTorch supplies device memory and the current stream.
+There is no fallback: if the library is missing, loading it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libkbest.so")
+
+KB_OK, KB_ERR_INVALID_ARG, KB_ERR_UNSUPPORTED, KB_ERR_WORKSPACE, KB_ERR_HIP = range(5)
+KB_F32, KB_BF16 = 0, 1
+KB_MAX_K = 16
+
+_lib = None
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int
+_SZ = ctypes.c_size_t
+
+# name -> (restype, argtypes), mirroring include/kbest.h
+SIGNATURES = {
+    "kb_abi_version": (_I, []),
+    "kb_status_string": (ctypes.c_char_p, [_I]),
+    "kb_last_error": (ctypes.c_char_p, []),
+    "kb_kbest_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I, _I]),
+    "kb_kbest_step": (_I, [_I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "kb_kbest_step_events": (_I, [_I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P,
+                                  _P, _P]),
+    "kb_compact_batch": (_I, [_I, _I, _P, _P, _P, _P, _P, _P, _P]),
+    "kb_gather_rows": (_I, [_I, _P, _P, _P, _P, _SZ, _P]),
+}
+
+
+class KBestError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        self.status = status
+        super().__init__(f"libkbest status {status}: {detail}")
+
+
+def lib() -> ctypes.CDLL:
+    """Load libkbest.so once; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                              "or python -m paper_1805_09863_amd._build")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != KB_OK:
+        raise KBestError(status, lib().kb_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return KB_F32
+    if t.dtype == torch.bfloat16:
+        return KB_BF16
+    raise TypeError(f"h and W must be float32 or bfloat16, got {t.dtype}")
+
+
+def _need(t: torch.Tensor, name: str, dtype=None, dim=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a tensor on the GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if dim is not None and t.dim() != dim:
+        raise ValueError(f"{name} must have {dim} dimensions")
+
+
+def abi_version() -> int:
+    return lib().kb_abi_version()
+
+
+def kbest_workspace_bytes(dtype: int, N: int, H: int, V: int, k: int, S: int) -> int:
+    return int(lib().kb_kbest_workspace_bytes(dtype, N, H, V, k, S))
+
+
+def workspace(nbytes: int, device=None) -> torch.Tensor:
+    """A device byte buffer usable as a workspace (torch allocations are 256-B aligned)."""
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device or "cuda")
+
+
+def kbest_step(h: torch.Tensor, W: torch.Tensor, b: torch.Tensor, prev_score: torch.Tensor,
+               sent_offsets: torch.Tensor, k: int, *, S: Optional[int] = None,
+               out: Optional[tuple] = None, ws: Optional[torch.Tensor] = None,
+               row_lse: Optional[torch.Tensor] = None, stream=None, events: Optional[tuple] = None):
+    """One decode step of the output layer: returns (token, parent, score), each S x k.
+
+    ``h`` is N x H, ``W`` is H x V (float32 or bfloat16, same type), ``b`` V
+    float32, ``prev_score`` N float32, ``sent_offsets`` S+1 int32, all on the
+    GPU.  ``out`` may supply preallocated (token, parent, score), ``ws`` a
+    workspace of at least ``kbest_workspace_bytes`` bytes, ``row_lse`` an N
+    float32 tensor to receive each row's log-sum-exp, ``events`` a pair of
+    raw hipEvent_t handles recorded around the projection kernel.
+    """
+    _need(h, "h", dim=2)
+    _need(W, "W", dtype=h.dtype, dim=2)
+    _need(b, "b", dtype=torch.float32, dim=1)
+    _need(prev_score, "prev_score", dtype=torch.float32, dim=1)
+    _need(sent_offsets, "sent_offsets", dtype=torch.int32, dim=1)
+    dt = _dtype_code(h)
+    N, H = h.shape
+    H2, V = W.shape
+    if H2 != H or b.shape[0] != V or prev_score.shape[0] != N:
+        raise ValueError("shape mismatch among h, W, b, prev_score")
+    S = sent_offsets.shape[0] - 1 if S is None else S
+    if sent_offsets.shape[0] != S + 1:
+        raise ValueError("sent_offsets must have S+1 entries")
+    dev = h.device
+    if out is None:
+        tok = torch.empty((S, k), dtype=torch.int32, device=dev)
+        par = torch.empty((S, k), dtype=torch.int32, device=dev)
+        sc = torch.empty((S, k), dtype=torch.float32, device=dev)
+    else:
+        tok, par, sc = out
+    need = kbest_workspace_bytes(dt, N, H, V, k, S)
+    if ws is None:
+        ws = workspace(need, dev)
+    if row_lse is not None:
+        _need(row_lse, "row_lse", dtype=torch.float32, dim=1)
+    L = lib()
+    args = [dt, N, H, V, k, S, _ptr(h), _ptr(W), _ptr(b), _ptr(prev_score), _ptr(sent_offsets),
+            _ptr(tok), _ptr(par), _ptr(sc), _ptr(row_lse), _ptr(ws), ws.numel() * ws.element_size(),
+            _stream(stream)]
+    if events is None:
+        _check(L.kb_kbest_step(*args))
+    else:
+        _check(L.kb_kbest_step_events(*args, ctypes.c_void_p(events[0]), ctypes.c_void_p(events[1])))
+    return tok, par, sc
+
+
+def compact_batch(alive: torch.Tensor, S: int, k: int, *, out: Optional[tuple] = None, stream=None):
+    """Stable removal of finished entries (Algorithm 2).
+
+    ``alive`` is S*k uint8 on the GPU.  Returns device tensors
+    (keep_idx[S*k], kept_count[1], new_sent_offsets[S+1], kept_sentence[S], new_S[1]);
+    only the first kept_count / new_S (+1) entries are meaningful.
+    """
+    _need(alive, "alive", dtype=torch.uint8)
+    if alive.numel() != S * k:
+        raise ValueError("alive must have S*k entries")
+    dev = alive.device
+    if out is None:
+        keep = torch.empty(max(S * k, 1), dtype=torch.int32, device=dev)
+        kept = torch.empty(1, dtype=torch.int32, device=dev)
+        noff = torch.empty(S + 1, dtype=torch.int32, device=dev)
+        ksent = torch.empty(max(S, 1), dtype=torch.int32, device=dev)
+        nS = torch.empty(1, dtype=torch.int32, device=dev)
+    else:
+        keep, kept, noff, ksent, nS = out
+    _check(lib().kb_compact_batch(S, k, _ptr(alive), _ptr(keep), _ptr(kept), _ptr(noff), _ptr(ksent),
+                                  _ptr(nS), _stream(stream)))
+    return keep, kept, noff, ksent, nS
+
+
+def gather_rows(src: torch.Tensor, idx: torch.Tensor, *, n_dev: Optional[torch.Tensor] = None,
+                n_max: Optional[int] = None, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """out[i] = src[idx[i]] for i < min(n_max, n_dev[0]) (rows of src along dim 0)."""
+    _need(src, "src")
+    _need(idx, "idx", dtype=torch.int32, dim=1)
+    n_max = idx.shape[0] if n_max is None else n_max
+    row_bytes = src[0].numel() * src.element_size() if src.shape[0] > 0 else 0
+    if out is None:
+        out = torch.empty((n_max,) + tuple(src.shape[1:]), dtype=src.dtype, device=src.device)
+    if n_max == 0:
+        return out
+    _check(lib().kb_gather_rows(n_max, _ptr(n_dev), _ptr(idx), _ptr(src), _ptr(out), row_bytes,
+                                _stream(stream)))
+    return out

@@ -1,0 +1,244 @@
+// Host side of libkbest: argument validation, launch planning, workspace
+// layout and the C entry points declared in include/kbest.h.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "../../include/kbest.h"
+#include "kb_common.hpp"
+
+namespace kb {
+hipError_t launch_k1_bf16_L256(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_bf16_L128(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_bf16_L32(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_f32_L256(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_f32_L128(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_f32_L32(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+
+hipError_t launch_k1(int bf16, int layout, int kc, dim3 grid, const K1Args& a, hipStream_t st) {
+  if (bf16) {
+    switch (layout) {
+      case K1_L256: return launch_k1_bf16_L256(kc, grid, a, st);
+      case K1_L128: return launch_k1_bf16_L128(kc, grid, a, st);
+      default: return launch_k1_bf16_L32(kc, grid, a, st);
+    }
+  }
+  switch (layout) {
+    case K1_L256: return launch_k1_f32_L256(kc, grid, a, st);
+    case K1_L128: return launch_k1_f32_L128(kc, grid, a, st);
+    default: return launch_k1_f32_L32(kc, grid, a, st);
+  }
+}
+}  // namespace kb
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+int ok() {
+  g_last_error.clear();
+  return KB_OK;
+}
+
+// The projection is planned for MI355X: 256 compute units, one fused
+// workgroup per CU (its LDS and registers allow no more).
+constexpr int kTargetCUs = 256;
+
+struct Plan {
+  int layout, kc, BH, BV;
+  int row_tiles, n_vtiles, P, tps;
+  size_t stats_off, lists_off, bytes;
+};
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+Plan make_plan(int dtype, int N, int V, int k) {
+  (void)dtype;
+  Plan p{};
+  if (N > 192) {
+    p.layout = kb::K1_L256;
+    p.BH = 256;
+    p.BV = 128;
+  } else if (N > 32) {
+    p.layout = kb::K1_L128;
+    p.BH = 128;
+    p.BV = 256;
+  } else {
+    p.layout = kb::K1_L32;
+    p.BH = 32;
+    p.BV = 512;
+  }
+  p.kc = k <= 4 ? 4 : (k <= 8 ? 8 : (k <= 12 ? 12 : 16));
+  p.row_tiles = (N + p.BH - 1) / p.BH;
+  p.n_vtiles = (V + p.BV - 1) / p.BV;
+  int P = kTargetCUs / (p.row_tiles > 0 ? p.row_tiles : 1);
+  if (P < 1) P = 1;
+  if (P > p.n_vtiles) P = p.n_vtiles;
+  if (P > 256) P = 256;
+  p.tps = (p.n_vtiles + P - 1) / P;
+  p.P = (p.n_vtiles + p.tps - 1) / p.tps;  // no empty split
+  p.stats_off = 0;
+  p.lists_off = align_up((size_t)p.P * N * sizeof(float2), 256);
+  p.bytes = align_up(p.lists_off + (size_t)p.P * N * k * sizeof(int2), 256);
+  return p;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+int validate_step(int dtype, int N, int H, int V, int k, int S) {
+  if (dtype != KB_F32 && dtype != KB_BF16) return fail(KB_ERR_INVALID_ARG, "unknown dtype %d", dtype);
+  if (N < 0 || S < 0) return fail(KB_ERR_INVALID_ARG, "negative N (%d) or S (%d)", N, S);
+  if ((N == 0) != (S == 0)) return fail(KB_ERR_INVALID_ARG, "N = %d and S = %d: both or neither must be 0", N, S);
+  if (H < 1 || V < 1) return fail(KB_ERR_INVALID_ARG, "H = %d and V = %d must be >= 1", H, V);
+  if (k < 1 || k > KB_MAX_K || k > V)
+    return fail(KB_ERR_INVALID_ARG, "k = %d outside [1, min(%d, V = %d)]", k, KB_MAX_K, V);
+  if (N < S) return fail(KB_ERR_INVALID_ARG, "N = %d < S = %d: every sentence needs a row", N, S);
+  if ((long long)N * k > INT_MAX || (long long)S * k > INT_MAX || (long long)H * V > (1LL << 40))
+    return fail(KB_ERR_UNSUPPORTED, "shape too large");
+  if ((long long)N * V > (1LL << 46)) return fail(KB_ERR_UNSUPPORTED, "N * V too large");
+  return KB_OK;
+}
+
+int kbest_step_impl(int dtype, int N, int H, int V, int k, int S, const void* h, const void* W, const float* b,
+                    const float* prev, const int32_t* off, int32_t* tok, int32_t* par, float* score,
+                    float* row_lse, void* ws, size_t ws_bytes, void* stream, void* ev0, void* ev1) {
+  int st = validate_step(dtype, N, H, V, k, S);
+  if (st != KB_OK) return st;
+  if (N == 0) return ok();
+  if (!h || !W || !b || !prev || !off || !tok || !par || !score)
+    return fail(KB_ERR_INVALID_ARG, "null input or output pointer");
+  const size_t esz = dtype == KB_BF16 ? 2 : 4;
+  if (!aligned(h, esz) || !aligned(W, esz) || !aligned(b, 4) || !aligned(prev, 4))
+    return fail(KB_ERR_INVALID_ARG, "h, W, b or prev misaligned for its element type");
+  const Plan p = make_plan(dtype, N, V, k);
+  if (!ws) return fail(KB_ERR_WORKSPACE, "workspace is null (%zu bytes needed)", p.bytes);
+  if (!aligned(ws, 256)) return fail(KB_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < p.bytes) return fail(KB_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, p.bytes);
+  if (p.P > 256) return fail(KB_ERR_UNSUPPORTED, "too many vocabulary splits");
+
+  const int vec = dtype == KB_BF16 ? 8 : 4;
+  kb::K1Args a1{};
+  a1.h = h;
+  a1.W = W;
+  a1.b = b;
+  a1.N = N;
+  a1.H = H;
+  a1.V = V;
+  a1.k = k;
+  a1.tps = p.tps;
+  a1.n_vtiles = p.n_vtiles;
+  a1.vec_ok = (H % vec == 0) && (V % vec == 0) && aligned(h, 16) && aligned(W, 16);
+  a1.stats = reinterpret_cast<float2*>((char*)ws + p.stats_off);
+  a1.lists = reinterpret_cast<int2*>((char*)ws + p.lists_off);
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+
+  if (ev0) {
+    hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev0), hs);
+    if (e != hipSuccess) return fail(KB_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+  }
+  hipError_t e = kb::launch_k1(dtype == KB_BF16, p.layout, p.kc, dim3(p.P, p.row_tiles), a1, hs);
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "projection kernel launch: %s", hipGetErrorString(e));
+  if (ev1) {
+    e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev1), hs);
+    if (e != hipSuccess) return fail(KB_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+  }
+
+  kb::K2Args a2{};
+  a2.stats = a1.stats;
+  a2.lists = a1.lists;
+  a2.P = p.P;
+  a2.N = N;
+  a2.V = V;
+  a2.k = k;
+  a2.S = S;
+  a2.prev = prev;
+  a2.off = off;
+  a2.tok = tok;
+  a2.par = par;
+  a2.score = score;
+  a2.row_lse = row_lse;
+  e = kb::launch_k2(a2, hs);
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "merge kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int kb_abi_version(void) { return KB_ABI_VERSION; }
+
+const char* kb_status_string(int s) {
+  switch (s) {
+    case KB_OK: return "ok";
+    case KB_ERR_INVALID_ARG: return "invalid argument";
+    case KB_ERR_UNSUPPORTED: return "unsupported";
+    case KB_ERR_WORKSPACE: return "workspace missing or too small";
+    case KB_ERR_HIP: return "HIP error";
+    default: return "unknown status";
+  }
+}
+
+const char* kb_last_error(void) { return g_last_error.c_str(); }
+
+size_t kb_kbest_workspace_bytes(int dtype, int N, int H, int V, int k, int S) {
+  if (validate_step(dtype, N, H, V, k, S) != KB_OK || N == 0) return 0;
+  return make_plan(dtype, N, V, k).bytes;
+}
+
+int kb_kbest_step(int dtype, int N, int H, int V, int k, int S, const void* h, const void* W, const float* b,
+                  const float* prev_score, const int32_t* sent_offsets, int32_t* out_token, int32_t* out_parent,
+                  float* out_score, float* out_row_lse, void* workspace, size_t workspace_bytes, void* stream) {
+  return kbest_step_impl(dtype, N, H, V, k, S, h, W, b, prev_score, sent_offsets, out_token, out_parent,
+                         out_score, out_row_lse, workspace, workspace_bytes, stream, nullptr, nullptr);
+}
+
+int kb_kbest_step_events(int dtype, int N, int H, int V, int k, int S, const void* h, const void* W,
+                         const float* b, const float* prev_score, const int32_t* sent_offsets, int32_t* out_token,
+                         int32_t* out_parent, float* out_score, float* out_row_lse, void* workspace,
+                         size_t workspace_bytes, void* stream, void* proj_begin_event, void* proj_end_event) {
+  return kbest_step_impl(dtype, N, H, V, k, S, h, W, b, prev_score, sent_offsets, out_token, out_parent,
+                         out_score, out_row_lse, workspace, workspace_bytes, stream, proj_begin_event,
+                         proj_end_event);
+}
+
+int kb_compact_batch(int S, int k, const uint8_t* alive, int32_t* keep_idx, int32_t* kept_count,
+                     int32_t* new_sent_offsets, int32_t* kept_sentence, int32_t* new_S, void* stream) {
+  if (S < 0) return fail(KB_ERR_INVALID_ARG, "S = %d < 0", S);
+  if (k < 1 || k > 1023) return fail(KB_ERR_INVALID_ARG, "k = %d outside [1, 1023]", k);
+  if ((long long)S * k > INT_MAX) return fail(KB_ERR_UNSUPPORTED, "S * k too large");
+  if (!kept_count || (S > 0 && (!alive || !keep_idx)))
+    return fail(KB_ERR_INVALID_ARG, "null alive, keep_idx or kept_count");
+  hipError_t e = kb::launch_compact(S, k, alive, keep_idx, kept_count, new_sent_offsets, kept_sentence, new_S,
+                                    reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "compaction kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int kb_gather_rows(int n_max, const int32_t* n_dev, const int32_t* idx, const void* src, void* dst,
+                   size_t row_bytes, void* stream) {
+  if (n_max < 0) return fail(KB_ERR_INVALID_ARG, "n_max = %d < 0", n_max);
+  if (row_bytes == 0 || row_bytes % 4 != 0) return fail(KB_ERR_INVALID_ARG, "row_bytes must be a positive multiple of 4");
+  if (row_bytes / 4 > INT_MAX) return fail(KB_ERR_UNSUPPORTED, "row too long");
+  if (n_max == 0) return ok();
+  if (!idx || !src || !dst) return fail(KB_ERR_INVALID_ARG, "null idx, src or dst");
+  if (!aligned(src, 4) || !aligned(dst, 4)) return fail(KB_ERR_INVALID_ARG, "src and dst must be 4-byte aligned");
+  hipError_t e = kb::launch_gather(n_max, n_dev, idx, src, dst, row_bytes, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "gather kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,101 @@
+"""The C ABI on the host: loading, exported symbols and argument validation.
+
+Every call here returns before any HIP work is enqueued, so no GPU is needed.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+kb = pytest.importorskip("paper_1805_09863_amd")
+from paper_1805_09863_amd import binding  # noqa: E402
+
+KB_OK, KB_ERR_INVALID_ARG, KB_ERR_UNSUPPORTED, KB_ERR_WORKSPACE = 0, 1, 2, 3
+FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: validation fails first
+
+
+def _header_functions(repo_root):
+    with open(os.path.join(repo_root, "include", "kbest.h")) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kb_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function(repo_root):
+    L = binding.lib()
+    names = _header_functions(repo_root)
+    assert len(names) >= 8
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in kbest.h but not exported"
+    assert set(names) == set(binding.SIGNATURES), "binding signatures out of sync with kbest.h"
+
+
+def test_abi_version_and_status_strings():
+    L = binding.lib()
+    assert L.kb_abi_version() == 1
+    for s in range(5):
+        assert L.kb_status_string(s)
+    assert L.kb_status_string(99) == b"unknown status"
+
+
+def test_workspace_bytes():
+    L = binding.lib()
+    big = L.kb_kbest_workspace_bytes(1, 3072, 1024, 90000, 12, 256)
+    # partials are far smaller than the N x V float32 scores they replace
+    assert 0 < big < 3072 * 90000 * 4 // 50
+    assert big % 256 == 0
+    assert L.kb_kbest_workspace_bytes(1, 3072, 1024, 90000, 12, 256) == big   # deterministic
+    assert L.kb_kbest_workspace_bytes(0, 0, 16, 100, 5, 0) == 0
+    assert L.kb_kbest_workspace_bytes(0, 5, 16, 100, 0, 1) == 0                # invalid k
+
+
+def _step(L, dtype=0, N=10, H=16, V=100, k=5, S=2, ptr=FAKE, ws=FAKE, ws_bytes=1 << 30, null_out=False):
+    out = None if null_out else ptr
+    return L.kb_kbest_step(dtype, N, H, V, k, S, ptr, ptr, ptr, ptr, ptr, out, out, out, None, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=7), KB_ERR_INVALID_ARG),
+    (dict(k=0), KB_ERR_INVALID_ARG),
+    (dict(k=17), KB_ERR_INVALID_ARG),
+    (dict(V=4, k=5), KB_ERR_INVALID_ARG),
+    (dict(N=1, S=2), KB_ERR_INVALID_ARG),
+    (dict(N=-1), KB_ERR_INVALID_ARG),
+    (dict(N=0, S=1), KB_ERR_INVALID_ARG),
+    (dict(H=0), KB_ERR_INVALID_ARG),
+    (dict(ptr=None), KB_ERR_INVALID_ARG),
+    (dict(null_out=True), KB_ERR_INVALID_ARG),
+    (dict(ws=None), KB_ERR_WORKSPACE),
+    (dict(ws_bytes=16), KB_ERR_WORKSPACE),
+    (dict(ws=ctypes.c_void_p(0x1010)), KB_ERR_WORKSPACE),
+    (dict(dtype=1, ptr=ctypes.c_void_p(0x1001)), KB_ERR_INVALID_ARG),
+])
+def test_kbest_step_validation(kw, status):
+    L = binding.lib()
+    assert _step(L, **kw) == status
+    assert L.kb_last_error()
+
+
+def test_empty_batch_is_noop():
+    L = binding.lib()
+    assert _step(L, N=0, S=0, ptr=None, ws=None, ws_bytes=0) == KB_OK
+    assert L.kb_last_error() == b""
+
+
+def test_compact_validation():
+    L = binding.lib()
+    assert L.kb_compact_batch(-1, 5, FAKE, FAKE, FAKE, None, None, None, None) == KB_ERR_INVALID_ARG
+    assert L.kb_compact_batch(4, 0, FAKE, FAKE, FAKE, None, None, None, None) == KB_ERR_INVALID_ARG
+    assert L.kb_compact_batch(4, 5, None, FAKE, FAKE, None, None, None, None) == KB_ERR_INVALID_ARG
+    assert L.kb_compact_batch(4, 5, FAKE, FAKE, None, None, None, None, None) == KB_ERR_INVALID_ARG
+    assert L.kb_compact_batch(1 << 30, 8, FAKE, FAKE, FAKE, None, None, None, None) == KB_ERR_UNSUPPORTED
+
+
+def test_gather_validation():
+    L = binding.lib()
+    assert L.kb_gather_rows(-1, None, FAKE, FAKE, FAKE, 16, None) == KB_ERR_INVALID_ARG
+    assert L.kb_gather_rows(4, None, FAKE, FAKE, FAKE, 6, None) == KB_ERR_INVALID_ARG
+    assert L.kb_gather_rows(4, None, None, FAKE, FAKE, 16, None) == KB_ERR_INVALID_ARG
+    assert L.kb_gather_rows(4, None, FAKE, ctypes.c_void_p(0x1002), FAKE, 16, None) == KB_ERR_INVALID_ARG
+    assert L.kb_gather_rows(0, None, None, None, None, 16, None) == KB_OK

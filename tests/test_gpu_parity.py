@@ -1,0 +1,130 @@
+"""GPU parity of kbest_step against the fp64 oracle, through the C ABI.
+
+Bar: scores within 1e-4 (float32) / 2e-2 (bf16) absolute in log space;
+token and parent exact wherever adjacent oracle scores differ by more than
+that; every device choice legal (rules (i)-(iii) of the comparison).
+"""
+import numpy as np
+import pytest
+import torch
+
+from synth import workloads as wl
+from tests.gpu_util import check, run_step, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def kb():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1805_09863_amd as kb
+    kb.lib()
+    return kb
+
+
+SMALL = [
+    # (N rows per sentence, H, V, k, dtype)  -- ragged tiles, tiny V, many splits
+    ([5], 256, 8000, 5, "f32"),
+    ([1], 64, 33, 1, "f32"),
+    ([3, 1, 4], 40, 517, 4, "f32"),           # H, V not multiples of the vector width
+    ([7, 2, 9, 1, 5], 96, 1500, 8, "bf16"),
+    ([12] * 6, 128, 4099, 12, "bf16"),
+    ([16] * 3, 64, 777, 16, "bf16"),
+    ([2] * 40, 200, 2048, 5, "bf16"),          # H not a multiple of 64
+    ([1] * 37, 33, 1003, 3, "bf16"),           # unaligned H and V: scalar loads
+    ([5] * 60, 256, 3000, 5, "f32"),           # 300 rows: large-N tile
+    ([5] * 80, 512, 1000, 5, "bf16"),          # 400 rows
+    ([9] * 30, 128, 20000, 9, "bf16"),
+    ([1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15, 16, 17], 64, 5000, 7, "f32"),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SMALL)))
+def test_small_shapes(kb, case):
+    rps, H, V, k, dt = SMALL[case]
+    inp = wl.make_step(H=H, V=V, k=k, rows_per_sentence=rps, dtype=dt, seed=500 + case, name=f"small{case}")
+    say(f"small case {case}: N={inp.N} H={H} V={V} k={k} {dt}")
+    out = run_step(kb, inp, row_lse=True)
+    rep, _ = check(inp, out)
+    say(f"  max score err {rep.max_score_err:.2e}, {rep.n_checked_idx} exact ranks")
+
+
+def test_zipf_bias_small(kb):
+    inp = wl.make_step(H=256, V=9000, k=12, S=20, beam=12, dtype="bf16", seed=77, bias="zipf", name="zipf")
+    check(inp, run_step(kb, inp, row_lse=True))
+
+
+def test_exact_twin_columns_lowest_index_wins(kb):
+    # Duplicate the best column of every row: the two logits are bitwise equal
+    # on the device, so the lower word must come first.
+    inp = wl.make_step(H=64, V=3000, k=4, S=8, beam=1, dtype="f32", seed=31, name="twins")
+    x = inp.h.astype(np.float64) @ inp.W.astype(np.float64) + inp.b
+    W, b = inp.W.copy(), inp.b.copy()
+    pairs = []
+    for r in range(inp.N):
+        j = int(np.argmax(x[r]))
+        t = (j + 1500) % inp.V
+        W[:, t] = W[:, j]
+        b[t] = b[j]
+        pairs.append((r, min(j, t), max(j, t)))
+    import dataclasses
+    inp = dataclasses.replace(inp, W=W, b=b)
+    tok, par, sc = run_step(kb, inp)
+    check(inp, (tok, par, sc))
+    for r, lo, hi in pairs:
+        row = [(int(tok[r, i]), float(sc[r, i])) for i in range(inp.k)]
+        toks = [t for t, _ in row]
+        if lo in toks and hi in toks:
+            assert toks.index(lo) < toks.index(hi), f"row {r}: twin order {row}"
+            assert row[toks.index(lo)][1] == row[toks.index(hi)][1]
+
+
+def test_duplicate_rows_lower_parent_wins(kb):
+    inp = wl.make_step(H=64, V=2000, k=6, S=4, beam=3, dtype="bf16", seed=41, name="duprows")
+    h = inp.h.copy()
+    prev = inp.prev.copy()
+    for s in range(inp.S):       # rows 1 and 2 of each sentence are identical
+        h[inp.off[s] + 2] = h[inp.off[s] + 1]
+        prev[inp.off[s] + 2] = prev[inp.off[s] + 1]
+    import dataclasses
+    inp = dataclasses.replace(inp, h=h, prev=prev)
+    tok, par, sc = run_step(kb, inp)
+    check(inp, (tok, par, sc))
+    for s in range(inp.S):
+        seen = set()
+        for r in range(inp.k):
+            p, t = int(par[s, r]) - int(inp.off[s]), int(tok[s, r])
+            if p == 2:
+                assert (1, t) in seen, f"sentence {s}: row-2 twin before row 1"
+            seen.add((p, t))
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2])
+def test_config_full(kb, cfg):
+    inp = wl.make_config(cfg)
+    say(f"config {cfg}: {inp.name} N={inp.N}")
+    out = run_step(kb, inp, row_lse=True)
+    rep, _ = check(inp, out)
+    say(f"  max score err {rep.max_score_err:.2e}, {rep.n_checked_idx} exact ranks")
+
+
+def test_config3_sampled(kb):
+    inp = wl.make_config(3)
+    say(f"config 3: {inp.name} N={inp.N}, oracle on sampled sentences")
+    out = run_step(kb, inp, row_lse=True)
+    sents = sorted(set(np.random.default_rng(3).choice(inp.S, 12, replace=False).tolist()) | {0, inp.S - 1})
+    rep, _ = check(inp, out, sentences=sents)
+    say(f"  max score err {rep.max_score_err:.2e}, {rep.n_checked_idx} exact ranks")
+
+
+def test_deterministic_and_workspace_poison(kb):
+    inp = wl.make_step(H=256, V=12000, k=12, S=30, beam=12, dtype="bf16", seed=55, name="det")
+    need = kb.kbest_workspace_bytes(kb.KB_BF16, inp.N, inp.H, inp.V, inp.k, inp.S)
+    ws = torch.full((need,), 0xFF, dtype=torch.uint8, device="cuda")
+    a = run_step(kb, inp, ws=ws)
+    ws.fill_(0x7F)
+    b = run_step(kb, inp, ws=ws)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+    check(inp, a)
