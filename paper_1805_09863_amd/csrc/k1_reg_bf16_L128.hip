@@ -1,0 +1,8 @@
+// Instantiations of the register-staged projection kernel: bf16 operands, layout L128.
+#include "k1_fused.hpp"
+
+namespace kb {
+hipError_t launch_k1_reg_bf16_L128(int kc, dim3 grid, const K1Args& a, hipStream_t st) {
+  return launch_k1_reg<true, LayL128>(kc, grid, a, st);
+}
+}  // namespace kb

@@ -152,6 +152,16 @@ __global__ __launch_bounds__(256) void k2_merge(K2Args a) {
   }
 }
 
+__global__ __launch_bounds__(256) void zero_u32(uint32_t* p, int n) {
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0u;
+}
+
+hipError_t launch_zero_u32(uint32_t* p, int n, hipStream_t st) {
+  const int blocks = n > 0 ? min((n + 255) / 256, 1024) : 1;
+  zero_u32<<<dim3(blocks), dim3(256), 0, st>>>(p, n);
+  return hipGetLastError();
+}
+
 hipError_t launch_k2(const K2Args& a, hipStream_t st) {
   if (a.P > 64 * K2_LPL || a.k > 16) return hipErrorInvalidValue;
   k2_merge<<<dim3(a.S), dim3(256), 0, st>>>(a);

@@ -26,6 +26,12 @@ __device__ __forceinline__ bool better(float a, int ia, float b, int ib) {
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Workgroup barrier for LDS only: waits for this wave's LDS operations, not
+// for its outstanding global->LDS DMA (a __syncthreads() fence would drain
+// the whole DMA ring).  The memory clobber keeps the compiler from moving
+// memory accesses across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // ---------------------------------------------------------------- K1
 struct K1Args {
   const void* h;      // N x H
@@ -37,12 +43,15 @@ struct K1Args {
   int vec_ok;         // 16-byte vector loads valid for h and W
   float2* stats;      // [P][N]   (max, sum of exp(x - max)) of each split
   int2* lists;        // [P][N][k] (score bits, word) of each split, best first
+  uint32_t* gthr;     // [N] shared per-row threshold (order-preserving key), zeroed per call
 };
 
 // Tile shapes of the fused projection kernel.
 enum K1Layout { K1_L256 = 0, K1_L128 = 1, K1_L32 = 2 };
 
-hipError_t launch_k1(int bf16, int layout, int kc, dim3 grid, const K1Args& a, hipStream_t st);
+// dma: the LDS-DMA pipeline (bf16, H % 32 == 0, V % 8 == 0, 16-byte aligned h and W)
+hipError_t launch_k1(int bf16, int dma, int layout, int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_zero_u32(uint32_t* p, int n, hipStream_t st);
 
 // ---------------------------------------------------------------- K2
 struct K2Args {

@@ -6,29 +6,39 @@
 
 #include <string>
 
-#include "../../include/kbest.h"
+#include "kbest.h"
 #include "kb_common.hpp"
 
 namespace kb {
-hipError_t launch_k1_bf16_L256(int kc, dim3 grid, const K1Args& a, hipStream_t st);
-hipError_t launch_k1_bf16_L128(int kc, dim3 grid, const K1Args& a, hipStream_t st);
-hipError_t launch_k1_bf16_L32(int kc, dim3 grid, const K1Args& a, hipStream_t st);
-hipError_t launch_k1_f32_L256(int kc, dim3 grid, const K1Args& a, hipStream_t st);
-hipError_t launch_k1_f32_L128(int kc, dim3 grid, const K1Args& a, hipStream_t st);
-hipError_t launch_k1_f32_L32(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_reg_bf16_L256(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_reg_bf16_L128(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_reg_bf16_L32(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_reg_f32_L256(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_reg_f32_L128(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_reg_f32_L32(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_dma_L256(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_dma_L128(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_dma_L32(int kc, dim3 grid, const K1Args& a, hipStream_t st);
 
-hipError_t launch_k1(int bf16, int layout, int kc, dim3 grid, const K1Args& a, hipStream_t st) {
+hipError_t launch_k1(int bf16, int dma, int layout, int kc, dim3 grid, const K1Args& a, hipStream_t st) {
+  if (dma) {
+    switch (layout) {
+      case K1_L256: return launch_k1_dma_L256(kc, grid, a, st);
+      case K1_L128: return launch_k1_dma_L128(kc, grid, a, st);
+      default: return launch_k1_dma_L32(kc, grid, a, st);
+    }
+  }
   if (bf16) {
     switch (layout) {
-      case K1_L256: return launch_k1_bf16_L256(kc, grid, a, st);
-      case K1_L128: return launch_k1_bf16_L128(kc, grid, a, st);
-      default: return launch_k1_bf16_L32(kc, grid, a, st);
+      case K1_L256: return launch_k1_reg_bf16_L256(kc, grid, a, st);
+      case K1_L128: return launch_k1_reg_bf16_L128(kc, grid, a, st);
+      default: return launch_k1_reg_bf16_L32(kc, grid, a, st);
     }
   }
   switch (layout) {
-    case K1_L256: return launch_k1_f32_L256(kc, grid, a, st);
-    case K1_L128: return launch_k1_f32_L128(kc, grid, a, st);
-    default: return launch_k1_f32_L32(kc, grid, a, st);
+    case K1_L256: return launch_k1_reg_f32_L256(kc, grid, a, st);
+    case K1_L128: return launch_k1_reg_f32_L128(kc, grid, a, st);
+    default: return launch_k1_reg_f32_L32(kc, grid, a, st);
   }
 }
 }  // namespace kb
@@ -60,7 +70,7 @@ constexpr int kTargetCUs = 256;
 struct Plan {
   int layout, kc, BH, BV;
   int row_tiles, n_vtiles, P, tps;
-  size_t stats_off, lists_off, bytes;
+  size_t stats_off, lists_off, gthr_off, bytes;
 };
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -92,7 +102,8 @@ Plan make_plan(int dtype, int N, int V, int k) {
   p.P = (p.n_vtiles + p.tps - 1) / p.tps;  // no empty split
   p.stats_off = 0;
   p.lists_off = align_up((size_t)p.P * N * sizeof(float2), 256);
-  p.bytes = align_up(p.lists_off + (size_t)p.P * N * k * sizeof(int2), 256);
+  p.gthr_off = align_up(p.lists_off + (size_t)p.P * N * k * sizeof(int2), 256);
+  p.bytes = align_up(p.gthr_off + (size_t)N * sizeof(uint32_t), 256);
   return p;
 }
 
@@ -143,13 +154,18 @@ int kbest_step_impl(int dtype, int N, int H, int V, int k, int S, const void* h,
   a1.vec_ok = (H % vec == 0) && (V % vec == 0) && aligned(h, 16) && aligned(W, 16);
   a1.stats = reinterpret_cast<float2*>((char*)ws + p.stats_off);
   a1.lists = reinterpret_cast<int2*>((char*)ws + p.lists_off);
+  a1.gthr = reinterpret_cast<uint32_t*>((char*)ws + p.gthr_off);
+  const int dma = dtype == KB_BF16 && H % 32 == 0 && a1.vec_ok;
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+
+  hipError_t e = kb::launch_zero_u32(a1.gthr, N, hs);
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "threshold reset kernel launch: %s", hipGetErrorString(e));
 
   if (ev0) {
     hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev0), hs);
     if (e != hipSuccess) return fail(KB_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
   }
-  hipError_t e = kb::launch_k1(dtype == KB_BF16, p.layout, p.kc, dim3(p.P, p.row_tiles), a1, hs);
+  e = kb::launch_k1(dtype == KB_BF16, dma, p.layout, p.kc, dim3(p.P, p.row_tiles), a1, hs);
   if (e != hipSuccess) return fail(KB_ERR_HIP, "projection kernel launch: %s", hipGetErrorString(e));
   if (ev1) {
     e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev1), hs);
