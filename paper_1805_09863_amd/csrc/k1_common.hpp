@@ -31,8 +31,9 @@ using LayL128 = Lay<4, 2, 2, 2>;  // 256 words x 128 rows
 using LayL32 = Lay<4, 1, 4, 1>;   // 512 words x 32 rows (few live rows)
 
 template <class L>
-struct SmemEpi {
-  float bias[L::BV];
+struct alignas(16) SmemEpi {
+  float bias[2][L::BV];     // bias of the current / next vocabulary tile
+  uint32_t tgk[2][L::BH];   // shared-threshold keys read at the tile's first stage
   float thr[L::BH];   // row's local threshold: k-th best score so far, or the seed
   int lcnt[256][L::WH];
   int flag[2];        // "some lane overflowed" of the current and the next round
@@ -113,14 +114,15 @@ struct Epilogue {
 
   // Shared threshold of this lane's rows (valid lower bounds of each row's
   // k-th best: k scores of the row are >= it).  Issued early, used in tile().
-  __device__ __forceinline__ void load_shared_thr(const K1Args& a, int h0, float (&tg)[WH]) {
+  // (Raw keys: decoding is deferred to the epilogue so that nothing waits on
+  // these loads, which would drain the DMA ring issued before them.)
+  __device__ __forceinline__ void load_shared_thr(const K1Args& a, int h0, uint32_t (&tg)[WH]) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wh = wave / NWV, col = lane & 31;
 #pragma unroll
     for (int hb = 0; hb < WH; ++hb) {
-      const int row = h0 + (wh * WH + hb) * 32 + col;
-      tg[hb] = row < a.N ? key2f(__hip_atomic_load(&a.gthr[row], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
-                         : kNoThr;
+      const int row = min(h0 + (wh * WH + hb) * 32 + col, a.N - 1);
+      tg[hb] = __hip_atomic_load(&a.gthr[row], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 
@@ -134,7 +136,7 @@ struct Epilogue {
   // One BV x BH tile of logits in acc (MFMA 32x32 layout: lane holds row
   // (hypothesis) col of each 32-block and 16 vocabulary entries).
   __device__ __forceinline__ void tile(f32x16 (&acc)[WV][WH], SmemEpi<L>& ep, const K1Args& a, int h0, int v0,
-                                       bool first, const float (&tg)[WH]) {
+                                       bool first, const uint32_t (&tg)[WH], const float* bias) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wv = wave % NWV, wh = wave / NWV;
     const int half = lane >> 5, col = lane & 31;
@@ -148,7 +150,7 @@ struct Epilogue {
       const int vl = (wv * WV + vb) * 32 + 4 * half;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float4 bb = *reinterpret_cast<const float4*>(&ep.bias[vl + 8 * i]);
+        const float4 bb = *reinterpret_cast<const float4*>(&bias[vl + 8 * i]);
 #pragma unroll
         for (int hb = 0; hb < WH; ++hb) {
           acc[vb][hb][4 * i + 0] += bb.x;
@@ -246,7 +248,7 @@ struct Epilogue {
         const int hl = (wh * WH + hb) * 32 + col;
         int c = 0;
         if (resume[hb] < DONE) {
-          const float t = fmaxf(ep.thr[hl], tg[hb]);
+          const float t = fmaxf(ep.thr[hl], key2f(tg[hb]));
           const int rs = resume[hb];
           int newres = DONE;
 #pragma unroll

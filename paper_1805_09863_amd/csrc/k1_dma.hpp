@@ -1,5 +1,5 @@
 // K1, DMA variant: the fused output-layer projection for bf16 h and W with
-// H % 32 == 0, V % 8 == 0 and 16-byte aligned operands (the production path).
+// H % 128 == 0, V % 8 == 0 and 16-byte aligned operands (the production path).
 //
 // Same work split and epilogue as the register-staged kernel; the difference
 // is how operands reach the matrix cores.  A ring of NS LDS stages (BK = 32
@@ -9,8 +9,9 @@
 //   * W keeps its V-contiguous layout in LDS; each 16-byte chunk of a row is
 //     XOR-swizzled by the row index, and MFMA A-fragments (8 consecutive k
 //     of one word) are built with the LDS transpose read ds_read_b64_tr_b16;
-//   * h is stored chunk-major ([k/8][row][8]) so that B-fragments are
-//     conflict-free 16-byte reads.
+//   * h rows are stored row-major, 64 bytes (BK = 32 states) per row, with
+//     the four 16-byte chunks XOR-swizzled by row; one DMA instruction reads
+//     16 rows x 64 contiguous bytes, and B-fragment reads stay conflict-free.
 // Each stage has its own __shared__ array, which lets the compiler see that
 // MFMA-side LDS reads never alias the DMA writes still in flight; the kernel
 // waits on the vector-memory counter itself (s_waitcnt vmcnt).
@@ -39,11 +40,16 @@ struct DmaGeom {
   static_assert(W_PER_WAVE % 64 == 0 || W_PER_WAVE < 64, "whole or partial DMA instructions");
   static_assert(H_PER_WAVE % 64 == 0 || H_PER_WAVE < 64, "whole or partial DMA instructions");
   static_assert(WCH >= 16, "the swizzle permutes 16 chunks");
+  static_assert(BK == 32, "h rows hold four 16-byte chunks per stage");
 };
 
 // XOR swizzle of the 16-byte chunks of W row r: rows r..r+3 read together by
 // one transpose read land on distinct banks.
 __device__ __forceinline__ int wswz(int r) { return 4 * (r & 3) + 2 * ((r >> 1) & 1); }
+
+// XOR swizzle of the four 16-byte chunks of an h row: the 16 rows read by a
+// 16-lane group at one logical chunk fall on 16 distinct 16-byte bank slots.
+__device__ __forceinline__ int hswz(int n) { return (n >> 2) & 3; }
 
 // s_waitcnt vmcnt(n) with expcnt / lgkmcnt left alone (gfx9 encoding).
 template <int N>
@@ -57,37 +63,66 @@ struct DmaKernel {
   using G = DmaGeom<L>;
   static constexpr int BV = L::BV, BH = L::BH, WV = L::WV, WH = L::WH, NWV = L::NWV;
   static constexpr int BK = G::BK;
+  // per-tile extras (bias, shared-threshold keys), issued with a tile's first stage
+  static constexpr int B_SLOTS = BV / 4, B_PER_WAVE = B_SLOTS / 4;  // float4 chunks
+  static constexpr int T_SLOTS = BH / 4, T_PER_WAVE = T_SLOTS / 4;  // uint4 chunks
+  static_assert(B_PER_WAVE >= 1 && B_PER_WAVE <= 64 && T_PER_WAVE >= 1 && T_PER_WAVE <= 64, "one extra op each");
 
-  // one DMA wave-instruction: 64 consecutive 16-byte LDS slots from base
-  __device__ __forceinline__ static void dma16(const void* g, KB_LDS void* lds_base) {
-    __builtin_amdgcn_global_load_lds(g, lds_base, 16, 0, 0);
-  }
+  // Per-lane parts of the DMA source addresses, fixed for the whole kernel.
+  struct Offs {
+    int wr[G::W_OPS], wc[G::W_OPS];  // W row within stage, word offset within tile
+    int hoff[G::H_OPS];              // h element offset (row * H + chunk)
+    int trow;                        // row whose shared-threshold key this lane copies
+  };
 
-  __device__ __forceinline__ static void issue(const K1Args& a, uint16_t* Wb, uint16_t* Hb, int h0, int v0,
-                                               int k0) {
+  __device__ __forceinline__ static void offsets(Offs& o, const K1Args& a, int h0) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const uint16_t* W = reinterpret_cast<const uint16_t*>(a.W);
-    const uint16_t* h = reinterpret_cast<const uint16_t*>(a.h);
 #pragma unroll
     for (int i = 0; i < G::W_OPS; ++i) {
-      const int slot0 = wave * G::W_PER_WAVE + i * 64;
-      if (G::W_PER_WAVE >= 64 || lane < G::W_PER_WAVE) {
-        const int s = slot0 + lane;
-        const int r = s / G::WCH, pc = s % G::WCH;
-        const int lc = pc ^ wswz(r);
-        const int v = min(v0 + lc * 8, a.V - 8);  // words >= V are masked in the epilogue
-        dma16(W + (size_t)(k0 + r) * a.V + v, (KB_LDS void*)(Wb + slot0 * 8));
-      }
+      const int s = wave * G::W_PER_WAVE + i * 64 + lane;
+      const int r = s / G::WCH, pc = s % G::WCH;
+      o.wr[i] = r;
+      o.wc[i] = (pc ^ wswz(r)) * 8;
     }
 #pragma unroll
     for (int i = 0; i < G::H_OPS; ++i) {
-      const int slot0 = wave * G::H_PER_WAVE + i * 64;
-      if (G::H_PER_WAVE >= 64 || lane < G::H_PER_WAVE) {
-        const int s = slot0 + lane;
-        const int kc = s / BH, n = s % BH;
-        const int row = min(h0 + n, a.N - 1);  // rows >= N are computed and never written
-        dma16(h + (size_t)row * a.H + k0 + kc * 8, (KB_LDS void*)(Hb + slot0 * 8));
+      // slot s = row * 4 + physical chunk; logical chunk = physical ^ hswz(row)
+      const int s = wave * G::H_PER_WAVE + i * 64 + lane;
+      const int n = s >> 2, pc = s & 3;
+      o.hoff[i] = min(h0 + n, a.N - 1) * a.H + (pc ^ hswz(n)) * 8;  // rows >= N: computed, never written
+    }
+    o.trow = h0 + (wave * T_PER_WAVE + lane) * 4;  // 4 keys per 16 bytes; the key array is padded to whole row tiles
+  }
+
+  // Stage (v0, k0) into LDS stage buffer sb (W then h); a tile's first stage
+  // also brings that tile's bias and shared-threshold keys into ep slot par.
+  __device__ __forceinline__ static void issue(const K1Args& a, const Offs& o, uint32_t sb, int v0, int k0,
+                                               uint32_t bias_lds, uint32_t tgk_lds) {
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint16_t* W = reinterpret_cast<const uint16_t*>(a.W) + (size_t)k0 * a.V;
+    const uint16_t* h = reinterpret_cast<const uint16_t*>(a.h) + k0;
+    const bool ragged = v0 + BV > a.V;
+#pragma unroll
+    for (int i = 0; i < G::W_OPS; ++i) {
+      if (G::W_PER_WAVE >= 64 || lane < G::W_PER_WAVE) {
+        int v = v0 + o.wc[i];
+        if (ragged) v = min(v, a.V - 8);  // words >= V are masked in the epilogue
+        dma16(W + (size_t)o.wr[i] * a.V + v, sb + (wave * G::W_PER_WAVE + i * 64) * 16);
       }
+    }
+    const uint32_t hb = sb + G::W_SLOTS * 16;
+#pragma unroll
+    for (int i = 0; i < G::H_OPS; ++i) {
+      if (G::H_PER_WAVE >= 64 || lane < G::H_PER_WAVE)
+        dma16(h + o.hoff[i], hb + (wave * G::H_PER_WAVE + i * 64) * 16);
+    }
+    if (k0 == 0) {
+      if (lane < B_PER_WAVE) {
+        const int v = min(v0 + (wave * B_PER_WAVE + lane) * 4, a.V - 4);  // words >= V are masked
+        dma16(a.b + v, bias_lds + wave * B_PER_WAVE * 16);
+      }
+      if (lane < T_PER_WAVE) dma16(a.gthr + o.trow, tgk_lds + wave * T_PER_WAVE * 16);
     }
   }
 
@@ -111,9 +146,11 @@ struct DmaKernel {
         __builtin_memcpy(&af[vb], t8, 16);
       }
 #pragma unroll
-      for (int hb = 0; hb < WH; ++hb)
-        bf[hb] = *reinterpret_cast<const bf16x8*>(
-            Hb + ((kk * 2 + (lane >> 5)) * BH + (wh * WH + hb) * 32 + (lane & 31)) * 8);
+      for (int hb = 0; hb < WH; ++hb) {
+        const int n = (wh * WH + hb) * 32 + (lane & 31);
+        const int kc = kk * 2 + (lane >> 5);
+        bf[hb] = *reinterpret_cast<const bf16x8*>(Hb + (n * 4 + (kc ^ hswz(n))) * 8);
+      }
 #pragma unroll
       for (int vb = 0; vb < WV; ++vb)
 #pragma unroll
@@ -127,46 +164,53 @@ template <class L, int KC>
 __global__ __launch_bounds__(256) void k1_dma(K1Args a) {
   using D = DmaKernel<L, KC>;
   using G = DmaGeom<L>;
-  constexpr int BV = L::BV, BH = L::BH, WV = L::WV, WH = L::WH;
+  constexpr int BV = L::BV, BH = L::BH, WV = L::WV, WH = L::WH, NWV = L::NWV;
   constexpr int WE = G::W_SLOTS * 8, HE = G::H_SLOTS * 8;  // bf16 elements per stage
-  __shared__ __attribute__((aligned(16))) uint16_t W0[WE], W1[WE], W2[WE], W3[WE];
-  __shared__ __attribute__((aligned(16))) uint16_t H0[HE], H1[HE], H2[HE], H3[HE];
-  __shared__ SmemEpi<L> ep;
+  // one __shared__ object per stage: W, then h
+  __shared__ __attribute__((aligned(16))) uint16_t S0[WE + HE], S1[WE + HE], S2[WE + HE], S3[WE + HE];
+  __shared__ __attribute__((aligned(16))) SmemEpi<L> ep;
   static_assert(G::NS == 4, "four named stage buffers");
+  // DMA accounting: every wave issues OPS instructions per stage, plus 2 with
+  // a tile's first stage.  Waiting for "at most 2*OPS outstanding" therefore
+  // always covers the oldest stage in flight (extra ops only make it stricter).
 
-  const int tid = threadIdx.x;
-  const int split = blockIdx.x;
-  const int h0 = blockIdx.y * BH;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int row_tile, split;
+  k1_cell(a, blockIdx.x, row_tile, split);
+  const int h0 = row_tile * BH;
   const int vt0 = split * a.tps;
   const int vt1 = min(vt0 + a.tps, a.n_vtiles);
-  const int nk = a.H / G::BK;
+  const int nk = a.H / G::BK;  // a multiple of 4: every tile starts on ring buffer 0
   const int total = (vt1 - vt0) * nk;
+  const uint32_t sbuf[4] = {lds_addr(S0), lds_addr(S1), lds_addr(S2), lds_addr(S3)};
 
   Epilogue<L, KC> epi;
   epi.init(ep, a.k);
+  typename D::Offs offs;
+  D::offsets(offs, a, h0);
 
-  // stage g covers tile vt0 + g / nk, state rows (g % nk) * BK ..
-  auto issue_g = [&](int g, uint16_t* Wb, uint16_t* Hb) {
-    const int t = g / nk, kt = g - t * nk;
-    D::issue(a, Wb, Hb, h0, (vt0 + t) * BV, kt * G::BK);
+  // next stage to issue: tile start iv0 (tile index it), state offset ik0
+  int iv0 = vt0 * BV, ik0 = 0, it = 0, issued = 0;
+  auto issue_next = [&](int buf) {
+    if (issued < total) {
+      D::issue(a, offs, sbuf[buf], iv0, ik0, lds_addr(&ep.bias[it & 1][0]), lds_addr(&ep.tgk[it & 1][0]));
+      ++issued;
+      ik0 += G::BK;
+      if (ik0 == a.H) {
+        ik0 = 0;
+        iv0 += BV;
+        ++it;
+      }
+    }
   };
-  issue_g(0, W0, H0);
-  if (total > 1) issue_g(1, W1, H1);
-  if (total > 2) issue_g(2, W2, H2);
+  issue_next(0);
+  issue_next(1);
+  issue_next(2);
 
-  float tg[WH];
-  epi.load_shared_thr(a, h0, tg);
-  f32x16 acc[WV][WH];
-#pragma unroll
-  for (int vb = 0; vb < WV; ++vb)
-#pragma unroll
-    for (int hb = 0; hb < WH; ++hb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[vb][hb][r] = 0.f;
-
-  int kt = 0, vt = vt0;
-  for (int g = 0; g < total; ++g) {
-    // wait for this thread's DMA of stage g (later issued stages may stay in flight)
+  // stage g: wait for this thread's DMA of g (later stages may stay in flight),
+  // barrier (all threads' data of g landed, stage g-1 consumed), refill the
+  // buffer of g-1 with stage g+3, compute on g.
+  auto wait_stage = [&](int g) {
     const int ahead = total - 1 - g;
     if (ahead >= 2)
       wait_vm<2 * G::OPS>();
@@ -174,40 +218,41 @@ __global__ __launch_bounds__(256) void k1_dma(K1Args a) {
       wait_vm<G::OPS>();
     else
       wait_vm<0>();
-    lds_barrier();  // every thread's stage-g data landed; stage g-1 fully consumed
-    if (kt == 0)
-      for (int i = tid; i < BV; i += 256) ep.bias[i] = (vt * BV + i < a.V) ? a.b[vt * BV + i] : 0.f;
-    switch (g & 3) {
-      case 0:
-        if (g + 3 < total) issue_g(g + 3, W3, H3);
-        D::compute(acc, W0, H0);
-        break;
-      case 1:
-        if (g + 3 < total) issue_g(g + 3, W0, H0);
-        D::compute(acc, W1, H1);
-        break;
-      case 2:
-        if (g + 3 < total) issue_g(g + 3, W1, H1);
-        D::compute(acc, W2, H2);
-        break;
-      default:
-        if (g + 3 < total) issue_g(g + 3, W2, H2);
-        D::compute(acc, W3, H3);
-        break;
+    lds_barrier();
+  };
+
+  int g = 0;
+  for (int vt = vt0; vt < vt1; ++vt) {
+    f32x16 acc[WV][WH];
+#pragma unroll
+    for (int vb = 0; vb < WV; ++vb)
+#pragma unroll
+      for (int hb = 0; hb < WH; ++hb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[vb][hb][r] = 0.f;
+    for (int kt = 0; kt < nk; kt += 4, g += 4) {
+      wait_stage(g);
+      issue_next(3);
+      D::compute(acc, S0, S0 + WE);
+      wait_stage(g + 1);
+      issue_next(0);
+      D::compute(acc, S1, S1 + WE);
+      wait_stage(g + 2);
+      issue_next(1);
+      D::compute(acc, S2, S2 + WE);
+      wait_stage(g + 3);
+      issue_next(2);
+      D::compute(acc, S3, S3 + WE);
     }
-    if (++kt == nk) {
-      lds_barrier();  // bias visible
-      epi.tile(acc, ep, a, h0, vt * BV, vt == vt0, tg);
-      kt = 0;
-      ++vt;
-      if (vt < vt1) epi.load_shared_thr(a, h0, tg);
+    // this tile's bias and keys landed with its first stage (waited for above)
+    const int par = (vt - vt0) & 1;
+    uint32_t tg[WH];
+    {
+      const int wh = wave / NWV, col = lane & 31;
 #pragma unroll
-      for (int vb = 0; vb < WV; ++vb)
-#pragma unroll
-        for (int hb = 0; hb < WH; ++hb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) acc[vb][hb][r] = 0.f;
+      for (int hb = 0; hb < WH; ++hb) tg[hb] = ep.tgk[par][(wh * WH + hb) * 32 + col];
     }
+    epi.tile(acc, ep, a, h0, vt * BV, vt == vt0, tg, ep.bias[par]);
   }
   epi.finish(ep, a, h0, split);
 }

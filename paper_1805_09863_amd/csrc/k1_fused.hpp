@@ -220,13 +220,14 @@ template <bool BF16, class L, int KC>
 __global__ __launch_bounds__(256) void k1_fused(K1Args a) {
   constexpr int BK = Ty<BF16>::BK;
   constexpr int BV = L::BV, BH = L::BH, WV = L::WV, WH = L::WH;
-  __shared__ SmemReg<BF16, L> sm;
+  __shared__ __attribute__((aligned(16))) SmemReg<BF16, L> sm;
   SmemEpi<L>& ep = sm.e;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wv = wave % L::NWV, wh = wave / L::NWV;
-  const int split = blockIdx.x;
-  const int h0 = blockIdx.y * BH;
+  int row_tile, split;
+  k1_cell(a, blockIdx.x, row_tile, split);
+  const int h0 = row_tile * BH;
   const int vt0 = split * a.tps;
   const int vt1 = min(vt0 + a.tps, a.n_vtiles);
   const int nk = (a.H + BK - 1) / BK;
@@ -239,7 +240,7 @@ __global__ __launch_bounds__(256) void k1_fused(K1Args a) {
 
   for (int vt = vt0; vt < vt1; ++vt) {
     const int v0 = vt * BV;
-    float tg[WH];
+    uint32_t tg[WH];
     epi.load_shared_thr(a, h0, tg);
     f32x16 acc[WV][WH];
 #pragma unroll
@@ -253,12 +254,12 @@ __global__ __launch_bounds__(256) void k1_fused(K1Args a) {
       __syncthreads();
       stage_store<BF16, L>(pf, sm, tid);
       if (kt == 0)
-        for (int i = tid; i < BV; i += 256) ep.bias[i] = (v0 + i < a.V) ? a.b[v0 + i] : 0.f;
+        for (int i = tid; i < BV; i += 256) ep.bias[0][i] = (v0 + i < a.V) ? a.b[v0 + i] : 0.f;
       __syncthreads();
       if (kt + 1 < nk) stage_load<BF16, L>(pf, a, h0, v0, (kt + 1) * BK, tid);
       stage_mma<BF16, L>(acc, sm, wv, wh, lane);
     }
-    epi.tile(acc, ep, a, h0, v0, vt == vt0, tg);
+    epi.tile(acc, ep, a, h0, v0, vt == vt0, tg, ep.bias[0]);
     if (vt + 1 < vt1) stage_load<BF16, L>(pf, a, h0, v0 + BV, 0, tid);
   }
   epi.finish(ep, a, h0, split);

@@ -32,6 +32,20 @@ __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_ex
 // memory accesses across it.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
+// LDS byte address of a __shared__ object.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// One global->LDS DMA wave-instruction (gfx950 global_load_lds_dwordx4): lane
+// i copies 16 bytes from its global address to LDS byte lds_base + 16 * i
+// (lds_base wave-uniform, in M0).  Issued from inline assembly so that the
+// compiler does not insert its own (conservative) waits for it; callers wait
+// with s_waitcnt vmcnt before reading the data.  One wait state after M0.
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_base) : "m0");
+}
+
 // ---------------------------------------------------------------- K1
 struct K1Args {
   const void* h;      // N x H
@@ -43,13 +57,37 @@ struct K1Args {
   int vec_ok;         // 16-byte vector loads valid for h and W
   float2* stats;      // [P][N]   (max, sum of exp(x - max)) of each split
   int2* lists;        // [P][N][k] (score bits, word) of each split, best first
-  uint32_t* gthr;     // [N] shared per-row threshold (order-preserving key), zeroed per call
+  uint32_t* gthr;     // [row_tiles * BH] shared per-row threshold keys (order-preserving), zeroed per call
+  int row_tiles;      // R
+  int P;              // vocabulary splits
+  int grp;            // row tiles per XCD group
 };
+
+// Workgroup -> (row tile, split).  Workgroups are dealt to the 8 XCDs
+// round-robin by block index; block b lands on XCD b % 8.  Each XCD is given
+// a contiguous run of cells of an ordering in which groups of `grp` row tiles
+// are walked split by split, so one XCD's L2 holds a few row tiles of h and
+// sees each W tile requested by all of them at about the same time.
+__device__ __forceinline__ void k1_cell(const K1Args& a, int b, int& row_tile, int& split) {
+  const int T = a.row_tiles * a.P;
+  const int x = b & 7, j = b >> 3;
+  const int c = x * (T >> 3) + min(x, T & 7) + j;
+  const int full = a.row_tiles / a.grp;            // complete row groups
+  const int gcells = a.grp * a.P;
+  int rg = c / gcells, gr = a.grp, q = c - rg * gcells;
+  if (rg >= full) {                                // the last, smaller group
+    gr = a.row_tiles - full * a.grp;
+    rg = full;
+    q = c - full * gcells;
+  }
+  split = q / gr;
+  row_tile = rg * a.grp + (q - split * gr);
+}
 
 // Tile shapes of the fused projection kernel.
 enum K1Layout { K1_L256 = 0, K1_L128 = 1, K1_L32 = 2 };
 
-// dma: the LDS-DMA pipeline (bf16, H % 32 == 0, V % 8 == 0, 16-byte aligned h and W)
+// dma: the LDS-DMA pipeline (bf16, H % 128 == 0, V % 8 == 0, 16-byte aligned h and W)
 hipError_t launch_k1(int bf16, int dma, int layout, int kc, dim3 grid, const K1Args& a, hipStream_t st);
 hipError_t launch_zero_u32(uint32_t* p, int n, hipStream_t st);
 

@@ -103,7 +103,7 @@ Plan make_plan(int dtype, int N, int V, int k) {
   p.stats_off = 0;
   p.lists_off = align_up((size_t)p.P * N * sizeof(float2), 256);
   p.gthr_off = align_up(p.lists_off + (size_t)p.P * N * k * sizeof(int2), 256);
-  p.bytes = align_up(p.gthr_off + (size_t)N * sizeof(uint32_t), 256);
+  p.bytes = align_up(p.gthr_off + (size_t)p.row_tiles * p.BH * sizeof(uint32_t), 256);
   return p;
 }
 
@@ -155,17 +155,20 @@ int kbest_step_impl(int dtype, int N, int H, int V, int k, int S, const void* h,
   a1.stats = reinterpret_cast<float2*>((char*)ws + p.stats_off);
   a1.lists = reinterpret_cast<int2*>((char*)ws + p.lists_off);
   a1.gthr = reinterpret_cast<uint32_t*>((char*)ws + p.gthr_off);
-  const int dma = dtype == KB_BF16 && H % 32 == 0 && a1.vec_ok;
+  a1.row_tiles = p.row_tiles;
+  a1.P = p.P;
+  a1.grp = p.row_tiles < 4 ? p.row_tiles : 4;
+  const int dma = dtype == KB_BF16 && H % 128 == 0 && a1.vec_ok && aligned(b, 16);
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
 
-  hipError_t e = kb::launch_zero_u32(a1.gthr, N, hs);
+  hipError_t e = kb::launch_zero_u32(a1.gthr, p.row_tiles * p.BH, hs);
   if (e != hipSuccess) return fail(KB_ERR_HIP, "threshold reset kernel launch: %s", hipGetErrorString(e));
 
   if (ev0) {
     hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev0), hs);
     if (e != hipSuccess) return fail(KB_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
   }
-  e = kb::launch_k1(dtype == KB_BF16, dma, p.layout, p.kc, dim3(p.P, p.row_tiles), a1, hs);
+  e = kb::launch_k1(dtype == KB_BF16, dma, p.layout, p.kc, dim3(p.P * p.row_tiles), a1, hs);
   if (e != hipSuccess) return fail(KB_ERR_HIP, "projection kernel launch: %s", hipGetErrorString(e));
   if (ev1) {
     e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev1), hs);
