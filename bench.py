@@ -36,7 +36,8 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
-K1_SOURCE = os.path.join(ROOT, "paper_1805_09863_amd", "csrc", "k1_fused.hpp")
+K1_SOURCES = [os.path.join(ROOT, "paper_1805_09863_amd", "csrc", f)
+              for f in ("kb_common.hpp", "k1_common.hpp", "k1_dma.hpp", "k1_fused.hpp")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k1_cfg3_hbm_traffic.txt")
 
 
@@ -70,8 +71,12 @@ class HipEvents:
 
 
 def k1_source_hash() -> str:
-    with open(K1_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the projection kernel's sources: counter summaries apply only to this code."""
+    h = hashlib.sha256()
+    for p in K1_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def read_traffic():
@@ -154,14 +159,18 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--cpu-sample-sentences", type=int, default=64)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode-loop", action="store_true")
+    ap.add_argument("--print-k1-hash", action="store_true", help="print the projection-kernel source hash and exit")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB three times (to scale HBM "
                          "byte counters against a kernel of known traffic), then exit")
     args = ap.parse_args()
+    if args.print_k1_hash:
+        print(k1_source_hash())
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the output layer shards by sentence or vocabulary; no multi-GPU path is built)", file=sys.stderr)
@@ -234,7 +243,7 @@ def main():
                    "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": read_traffic(),
-                     "kernel": "k1_fused (projection + bias + softmax statistics + per-split k-best)",
+                     "kernel": "k1_dma (projection + bias + softmax statistics + per-split k-best)",
                      "kernel_ms": k1_mean, "flops_per_launch": flops},
     }
     tr = result["roofline"]["traffic"]
