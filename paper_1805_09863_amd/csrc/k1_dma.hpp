@@ -21,9 +21,6 @@
 
 namespace kb {
 
-#define KB_LDS __attribute__((address_space(3)))
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-
 template <class L>
 struct DmaGeom {
   static constexpr int BK = 32;                 // K per stage
@@ -42,21 +39,6 @@ struct DmaGeom {
   static_assert(WCH >= 16, "the swizzle permutes 16 chunks");
   static_assert(BK == 32, "h rows hold four 16-byte chunks per stage");
 };
-
-// XOR swizzle of the 16-byte chunks of W row r: rows r..r+3 read together by
-// one transpose read land on distinct banks.
-__device__ __forceinline__ int wswz(int r) { return 4 * (r & 3) + 2 * ((r >> 1) & 1); }
-
-// XOR swizzle of the four 16-byte chunks of an h row: the 16 rows read by a
-// 16-lane group at one logical chunk fall on 16 distinct 16-byte bank slots.
-__device__ __forceinline__ int hswz(int n) { return (n >> 2) & 3; }
-
-// s_waitcnt vmcnt(n) with expcnt / lgkmcnt left alone (gfx9 encoding).
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
 
 template <class L, int KC>
 struct DmaKernel {

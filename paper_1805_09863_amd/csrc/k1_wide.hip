@@ -1,0 +1,14 @@
+// Instantiations of the wide (256 x 256 tile) bf16 projection kernel.
+#include "k1_wide.hpp"
+
+namespace kb {
+hipError_t launch_k1_wide(int kc, dim3 grid, const K1Args& a, hipStream_t st) {
+  switch (kc) {
+    case 4: return launch_k1_wide_kc<4>(grid, a, st);
+    case 8: return launch_k1_wide_kc<8>(grid, a, st);
+    case 12: return launch_k1_wide_kc<12>(grid, a, st);
+    case 16: return launch_k1_wide_kc<16>(grid, a, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+}  // namespace kb

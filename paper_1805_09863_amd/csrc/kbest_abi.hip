@@ -19,10 +19,12 @@ hipError_t launch_k1_reg_f32_L32(int kc, dim3 grid, const K1Args& a, hipStream_t
 hipError_t launch_k1_dma_L256(int kc, dim3 grid, const K1Args& a, hipStream_t st);
 hipError_t launch_k1_dma_L128(int kc, dim3 grid, const K1Args& a, hipStream_t st);
 hipError_t launch_k1_dma_L32(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_wide(int kc, dim3 grid, const K1Args& a, hipStream_t st);
 
 hipError_t launch_k1(int bf16, int dma, int layout, int kc, dim3 grid, const K1Args& a, hipStream_t st) {
   if (dma) {
     switch (layout) {
+      case K1_W256: return launch_k1_wide(kc, grid, a, st);
       case K1_L256: return launch_k1_dma_L256(kc, grid, a, st);
       case K1_L128: return launch_k1_dma_L128(kc, grid, a, st);
       default: return launch_k1_dma_L32(kc, grid, a, st);
@@ -75,10 +77,19 @@ struct Plan {
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-Plan make_plan(int dtype, int N, int V, int k) {
-  (void)dtype;
+// Rows from which the 256 x 256 tile pays off (it needs the DMA pipeline).
+constexpr int kWideMinRows = 513;
+
+// Shapes the DMA pipeline accepts, pointer alignment aside.
+bool dma_shape(int dtype, int H, int V) { return dtype == KB_BF16 && H % 128 == 0 && V % 8 == 0; }
+
+Plan make_plan(int dtype, int N, int H, int V, int k, bool dma) {
   Plan p{};
-  if (N > 192) {
+  if (dma && N >= kWideMinRows && dma_shape(dtype, H, V)) {
+    p.layout = kb::K1_W256;
+    p.BH = 256;
+    p.BV = 256;
+  } else if (N > 192) {
     p.layout = kb::K1_L256;
     p.BH = 256;
     p.BV = 128;
@@ -105,6 +116,12 @@ Plan make_plan(int dtype, int N, int V, int k) {
   p.gthr_off = align_up(p.lists_off + (size_t)p.P * N * k * sizeof(int2), 256);
   p.bytes = align_up(p.gthr_off + (size_t)p.row_tiles * p.BH * sizeof(uint32_t), 256);
   return p;
+}
+
+// Workspace for a shape: enough for whichever plan the pointers' alignment selects.
+size_t workspace_bytes(int dtype, int N, int H, int V, int k) {
+  const size_t a = make_plan(dtype, N, H, V, k, true).bytes, b = make_plan(dtype, N, H, V, k, false).bytes;
+  return a > b ? a : b;
 }
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
@@ -134,13 +151,16 @@ int kbest_step_impl(int dtype, int N, int H, int V, int k, int S, const void* h,
   const size_t esz = dtype == KB_BF16 ? 2 : 4;
   if (!aligned(h, esz) || !aligned(W, esz) || !aligned(b, 4) || !aligned(prev, 4))
     return fail(KB_ERR_INVALID_ARG, "h, W, b or prev misaligned for its element type");
-  const Plan p = make_plan(dtype, N, V, k);
-  if (!ws) return fail(KB_ERR_WORKSPACE, "workspace is null (%zu bytes needed)", p.bytes);
+  const int vec = dtype == KB_BF16 ? 8 : 4;
+  const bool vec_ok = (H % vec == 0) && (V % vec == 0) && aligned(h, 16) && aligned(W, 16);
+  const bool dma = dma_shape(dtype, H, V) && vec_ok && aligned(b, 16);
+  const Plan p = make_plan(dtype, N, H, V, k, dma);
+  const size_t need = workspace_bytes(dtype, N, H, V, k);
+  if (!ws) return fail(KB_ERR_WORKSPACE, "workspace is null (%zu bytes needed)", need);
   if (!aligned(ws, 256)) return fail(KB_ERR_WORKSPACE, "workspace must be 256-byte aligned");
-  if (ws_bytes < p.bytes) return fail(KB_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, p.bytes);
+  if (ws_bytes < need) return fail(KB_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
   if (p.P > 256) return fail(KB_ERR_UNSUPPORTED, "too many vocabulary splits");
 
-  const int vec = dtype == KB_BF16 ? 8 : 4;
   kb::K1Args a1{};
   a1.h = h;
   a1.W = W;
@@ -151,14 +171,13 @@ int kbest_step_impl(int dtype, int N, int H, int V, int k, int S, const void* h,
   a1.k = k;
   a1.tps = p.tps;
   a1.n_vtiles = p.n_vtiles;
-  a1.vec_ok = (H % vec == 0) && (V % vec == 0) && aligned(h, 16) && aligned(W, 16);
+  a1.vec_ok = vec_ok;
   a1.stats = reinterpret_cast<float2*>((char*)ws + p.stats_off);
   a1.lists = reinterpret_cast<int2*>((char*)ws + p.lists_off);
   a1.gthr = reinterpret_cast<uint32_t*>((char*)ws + p.gthr_off);
   a1.row_tiles = p.row_tiles;
   a1.P = p.P;
   a1.grp = p.row_tiles < 4 ? p.row_tiles : 4;
-  const int dma = dtype == KB_BF16 && H % 128 == 0 && a1.vec_ok && aligned(b, 16);
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
 
   hipError_t e = kb::launch_zero_u32(a1.gthr, p.row_tiles * p.BH, hs);
@@ -215,7 +234,7 @@ const char* kb_last_error(void) { return g_last_error.c_str(); }
 
 size_t kb_kbest_workspace_bytes(int dtype, int N, int H, int V, int k, int S) {
   if (validate_step(dtype, N, H, V, k, S) != KB_OK || N == 0) return 0;
-  return make_plan(dtype, N, V, k).bytes;
+  return workspace_bytes(dtype, N, H, V, k);
 }
 
 int kb_kbest_step(int dtype, int N, int H, int V, int k, int S, const void* h, const void* W, const float* b,

@@ -50,6 +50,31 @@ def test_small_shapes(kb, case):
     say(f"  max score err {rep.max_score_err:.2e}, {rep.n_checked_idx} exact ranks")
 
 
+# Shapes for the 256 x 256-tile projection kernel (bf16, H % 128 == 0,
+# V % 8 == 0, at least 513 rows): ragged last row and word tiles, a last
+# word tile holding only 8 words, the shortest state (4 stages per tile),
+# one tile per split, k = 1 and k = 16.
+WIDE = [
+    ([5] * 120, 128, 2056, 5),                 # N 600; last word tile holds 8 words
+    ([12] * 50, 256, 5000, 12),                # N 600; ragged word tile of 136
+    ([16] * 40, 384, 3000, 16),                # k = 16, 12 stages per tile
+    ([1] * 700, 128, 9000, 1),                 # beam 1, k = 1
+    ([4] * 256, 1024, 30000, 4),               # four whole row tiles
+    ([3] * 250 + [2] * 20, 256, 6216, 8),      # mixed beams, N 790
+    ([6] * 100, 128, 1024, 6),                 # 4 word tiles: one tile per split
+]
+
+
+@pytest.mark.parametrize("case", range(len(WIDE)))
+def test_wide_tile_shapes(kb, case):
+    rps, H, V, k = WIDE[case]
+    inp = wl.make_step(H=H, V=V, k=k, rows_per_sentence=rps, dtype="bf16", seed=900 + case, name=f"wide{case}")
+    say(f"wide case {case}: N={inp.N} H={H} V={V} k={k}")
+    out = run_step(kb, inp, row_lse=True)
+    rep, _ = check(inp, out)
+    say(f"  max score err {rep.max_score_err:.2e}, {rep.n_checked_idx} exact ranks")
+
+
 def test_zipf_bias_small(kb):
     inp = wl.make_step(H=256, V=9000, k=12, S=20, beam=12, dtype="bf16", seed=77, bias="zipf", name="zipf")
     check(inp, run_step(kb, inp, row_lse=True))
