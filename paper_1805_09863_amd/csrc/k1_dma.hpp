@@ -124,8 +124,7 @@ struct DmaKernel {
         const int a1 = a0 + 4 * BV;  // rows r0 + 4: same swizzle
         const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((KB_LDS s16x4*)(Wb + a0));
         const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((KB_LDS s16x4*)(Wb + a1));
-        const short t8[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        __builtin_memcpy(&af[vb], t8, 16);
+        af[vb] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
       }
 #pragma unroll
       for (int hb = 0; hb < WH; ++hb) {

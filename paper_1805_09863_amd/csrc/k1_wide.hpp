@@ -44,29 +44,41 @@ struct WideGeom {
   static constexpr int WE = BK * BV;  // bf16 elements of W per stage
   static constexpr int HE = BH * BK;  // bf16 elements of h per stage
   static constexpr int OPS = 8;       // DMA instructions per wave per stage
-  static constexpr int CAP = 12;      // candidate slots per row per round
+  static constexpr int DMA_SLOT0 = 6; // first MFMA (of a stage's second 16) followed by a DMA instruction
+  static constexpr int CAPH = 5;      // candidate slots per row and holder per round
   static constexpr int DONE = 64;     // "no pending candidates" position
 };
 
 struct alignas(16) WideEpi {
   float bias[2][WideGeom::BV];    // bias of the current / next tile (DMA)
-  uint32_t tgk[2][WideGeom::BH];  // shared-threshold keys of the current / next tile (DMA)
+  uint32_t tgk[2][WideGeom::BH];  // shared-threshold keys read for the current / next tile (DMA)
   float thr[WideGeom::BH];        // row's local threshold: its k-th best so far, or the seed
-  int cnt[WideGeom::BH];          // candidates appended to the row this round
+  uint32_t cnt[WideGeom::BH];     // candidates each holder appended to the row this round (one byte each)
   int flag[4];                    // "a lane could not append" of this and the next round
   union {
-    int2 cand[WideGeom::BH][WideGeom::CAP];  // (score bits, word) appended this round
-    float red[WideGeom::BH][8];              // seeds, then the per-holder statistics
+    struct {
+      float x[WideGeom::BH][4][WideGeom::CAPH];    // scores appended this round, per row and holder
+      uint8_t p[WideGeom::BH][4][WideGeom::CAPH];  // their positions (0..63) among the holder's scores
+    } c;
+    float red[WideGeom::BH][16];  // seeds, then the per-holder statistics
   } u;
 };
 
-// One global->LDS DMA wave-instruction with a wave-uniform base (SGPR pair)
-// and a per-lane 32-bit byte offset: lane i copies 16 bytes from
-// base + voff to LDS byte lds_base + 16 i.
-__device__ __forceinline__ void dma16_so(uint32_t voff, const void* sbase, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase),
-               "s"(lds_base)
-               : "m0");
+// Global->LDS DMA with a wave-uniform base (SGPR pair) and a per-lane 32-bit
+// byte offset: lane i copies 16 bytes from base + voff + OFF to LDS byte
+// M0 + OFF + 16 i (the immediate offset shifts both addresses).
+// Group form: M0 is set once (set_m0) for up to four DMA instructions whose
+// immediate offsets (0..3072) shift both the global and the LDS address; the
+// per-lane offset is pre-compensated by -OFF.
+__device__ __forceinline__ void set_m0(uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0" ::"s"(__builtin_amdgcn_readfirstlane(lds_base)) : "m0");
+}
+template <int OFF>
+__device__ __forceinline__ void dma16_off(uint32_t voff, const void* sbase) {
+  const uint64_t p = reinterpret_cast<uint64_t>(sbase);
+  const uint64_t u = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(p >> 32)) << 32) |
+                     (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)p);
+  asm volatile("global_load_lds_dwordx4 %0, %1 offset:%2" ::"v"(voff), "s"(reinterpret_cast<const void*>(u)), "i"(OFF));
 }
 
 // Marks an accumulator block as redefined in place (it stays in the
@@ -81,6 +93,13 @@ __device__ __forceinline__ void opaque(f32x16& x) { asm volatile("" : "+a"(x)); 
 // VGPRs at once).
 __device__ __forceinline__ void done(float x) { asm volatile("" ::"v"(x)); }
 __device__ __forceinline__ void done(int x) { asm volatile("" ::"v"(x)); }
+
+// 64-bit order key of a (score, word) candidate: higher score first, then
+// lower word (the strict-'>' scans of the paper).  -0 is folded into +0 so
+// that equal scores compare equal.
+__device__ __forceinline__ uint64_t cand_key(float x, int word) {
+  return ((uint64_t)f2key(x + 0.0f) << 32) | (uint32_t)~(uint32_t)word;
+}
 
 __device__ __forceinline__ float max4(const f32x16& x, int q) {
   return fmaxf(fmax3(x[4 * q], x[4 * q + 1], x[4 * q + 2]), x[4 * q + 3]);
@@ -112,52 +131,73 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
   // W slot s = 256 wave + 64 i + lane: stage row r = s / 32, physical chunk
   // s % 32 holding logical chunk (s % 32) ^ wswz(r).
   // h slot s: row n = s / 4, physical chunk s % 4 holding chunk (s % 4) ^ hswz(n).
+  // Offsets are pre-compensated for the immediate offset 1024 i of DMA
+  // instruction i (they stay >= 0: r >= 2 i and V >= 256; n >= 16 i and H >= 128).
   uint32_t woff[4], hoff[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int r = wave * 8 + i * 2 + half;
-    woff[i] = (uint32_t)r * (uint32_t)a.V * 2u + (uint32_t)((col ^ wswz(r)) * 16);
+    woff[i] = (uint32_t)r * (uint32_t)a.V * 2u + (uint32_t)((col ^ wswz(r)) * 16) - 1024u * i;
     const int n = wave * 64 + i * 16 + (lane >> 2);
-    hoff[i] = (uint32_t)min(h0 + n, a.N - 1) * (uint32_t)a.H * 2u + (uint32_t)(((lane & 3) ^ hswz(n)) * 16);
+    hoff[i] = (uint32_t)min(h0 + n, a.N - 1) * (uint32_t)a.H * 2u + (uint32_t)(((lane & 3) ^ hswz(n)) * 16) - 1024u * i;
   }
 
-  auto issue = [&](uint16_t* buf, int v0, int k0, int par) {
-    const uint32_t sb = lds_addr(buf);
-    const char* Wp = reinterpret_cast<const char*>(a.W) + ((size_t)k0 * a.V + v0) * 2;
-    const char* Hp = reinterpret_cast<const char*>(a.h) + (size_t)k0 * 2;
-    if (v0 + BV <= a.V) {
+  // ---- the next stage to issue: tile start iv0 (tile it), state offset ik0;
+  // wsrc / hsrc point at its first W row / h column; wdma are the W offsets of
+  // its tile (clamped for the last, ragged tile: words >= V read word V - 8..
+  // instead, which start at -inf).
+  int iv0 = vt0 * BV, ik0 = 0, it = 0, issued = 0;
+  const char* wsrc = reinterpret_cast<const char*>(a.W) + (size_t)iv0 * 2;
+  const char* hsrc = reinterpret_cast<const char*>(a.h);
+  uint32_t wdma[4];
+  auto set_wdma = [&]() {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) dma16_so(woff[i], Wp, sb + (wave * 256 + i * 64) * 16);
-    } else {  // last, ragged tile: words >= V read word V - 8.. instead (they start at -inf)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < 4; ++i) {
+      wdma[i] = woff[i];
+      if (iv0 + BV > a.V) {
         const int r = wave * 8 + i * 2 + half;
-        const int w = min(v0 + (col ^ wswz(r)) * 8, a.V - 8) - v0;
-        dma16_so((uint32_t)r * (uint32_t)a.V * 2u + (uint32_t)w * 2u, Wp, sb + (wave * 256 + i * 64) * 16);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) dma16_so(hoff[i], Hp, sb + WE * 2 + (wave * 256 + i * 64) * 16);
-    if (k0 == 0) {  // the tile's bias and shared-threshold keys ride with its first stage
-      if (wave == 0) {
-        dma16(a.b + min(v0 + lane * 4, a.V - 4), lds_addr(&ep.bias[par][0]));
-      } else if (wave == 1) {
-        dma16(a.gthr + h0 + lane * 4, lds_addr(&ep.tgk[par][0]));
+        wdma[i] = (uint32_t)r * (uint32_t)a.V * 2u + (uint32_t)(min(iv0 + (col ^ wswz(r)) * 8, a.V - 8) - iv0) * 2u -
+                  1024u * i;
       }
     }
   };
-
-  int iv0 = vt0 * BV, ik0 = 0, it = 0, issued = 0;
-  auto issue_next = [&](uint16_t* buf) {
+  set_wdma();
+  // DMA instruction i (0..7) of the next stage into buffer buf: W rows (i < 4)
+  // or h rows; i = 0 and 4 set M0 for their group of four
+  auto dma_part = [&](uint16_t* buf, int i) {
+    const uint32_t sb = lds_addr(buf) + wave * 4096 + (i < 4 ? 0 : WE * 2);
+    if ((i & 3) == 0) set_m0(sb);
+    switch (i) {
+      case 0: dma16_off<0>(wdma[0], wsrc); break;
+      case 1: dma16_off<1024>(wdma[1], wsrc); break;
+      case 2: dma16_off<2048>(wdma[2], wsrc); break;
+      case 3: dma16_off<3072>(wdma[3], wsrc); break;
+      case 4: dma16_off<0>(hoff[0], hsrc); break;
+      case 5: dma16_off<1024>(hoff[1], hsrc); break;
+      case 6: dma16_off<2048>(hoff[2], hsrc); break;
+      default: dma16_off<3072>(hoff[3], hsrc); break;
+    }
+  };
+  auto dma_finish = [&]() {  // the tile's bias rides with its first stage
+    if (ik0 == 0 && wave == 0) dma16(a.b + min(iv0 + lane * 4, a.V - 4), lds_addr(&ep.bias[it & 1][0]));
+    ++issued;
+    ik0 += BK;
+    wsrc += (size_t)BK * a.V * 2;
+    hsrc += BK * 2;
+    if (ik0 == a.H) {
+      ik0 = 0;
+      iv0 += BV;
+      ++it;
+      wsrc = reinterpret_cast<const char*>(a.W) + (size_t)iv0 * 2;
+      hsrc = reinterpret_cast<const char*>(a.h);
+      set_wdma();
+    }
+  };
+  auto issue_whole = [&](uint16_t* buf) {
     if (issued < total) {
-      issue(buf, iv0, ik0, it & 1);
-      ++issued;
-      ik0 += BK;
-      if (ik0 == a.H) {
-        ik0 = 0;
-        iv0 += BV;
-        ++it;
-      }
+#pragma unroll
+      for (int i = 0; i < G::OPS; ++i) dma_part(buf, i);
+      dma_finish();
     }
   };
 
@@ -178,27 +218,36 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) boff[kk] = (uint32_t)(WE + n * 32 + (((kk * 2 + half) ^ hswz(n)) * 8)) * 2u;
   }
-  auto load_frags = [&](const uint16_t* buf, int kk, bf16x8(&fa)[4], bf16x8(&fb)[4]) {
+  // A fragment of block vb = two transpose reads (states 0-3 and 4-7 of the
+  // lane's half); B fragment of block hb = one 16-byte read.
+  struct Frag {
+    s16x4 lo[4], hi[4];
+    bf16x8 b[4];
+  };
+  // read u (0..11) of a fragment set, in the order the MFMAs consume them:
+  // b0, lo0, hi0, b1, b2, b3, lo1, hi1, lo2, hi2, lo3, hi3
+  auto rd = [&](const uint16_t* buf, int kk, int u, Frag& f) {
     const KB_LDS char* base = (const KB_LDS char*)(const KB_LDS void*)buf;
-#pragma unroll
-    for (int vb = 0; vb < 4; ++vb) {
-      const KB_LDS char* p = base + aoff[vb] + kk * 16 * BV * 2;
-      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((KB_LDS s16x4*)p);
-      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((KB_LDS s16x4*)(p + 4 * BV * 2));
-      const short t8[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-      __builtin_memcpy(&fa[vb], t8, 16);
+    constexpr int kind[12] = {2, 0, 1, 2, 2, 2, 0, 1, 0, 1, 0, 1};  // 0 lo, 1 hi, 2 b
+    constexpr int blk[12] = {0, 0, 0, 1, 2, 3, 1, 1, 2, 2, 3, 3};
+    const int x = blk[u];
+    if (kind[u] == 2) {
+      f.b[x] = *(const KB_LDS bf16x8*)(base + boff[kk] + x * 2048);
+    } else {
+      const KB_LDS char* p = base + aoff[x] + kk * 16 * BV * 2 + kind[u] * 4 * BV * 2;
+      const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((KB_LDS s16x4*)p);
+      if (kind[u] == 0)
+        f.lo[x] = v;
+      else
+        f.hi[x] = v;
     }
-#pragma unroll
-    for (int hb = 0; hb < 4; ++hb) fb[hb] = *(const KB_LDS bf16x8*)(base + boff[kk] + hb * 2048);
   };
 
   f32x16 acc[4][4];
-  auto mfma16 = [&](const bf16x8(&fa)[4], const bf16x8(&fb)[4]) {
-#pragma unroll
-    for (int vb = 0; vb < 4; ++vb)
-#pragma unroll
-      for (int hb = 0; hb < 4; ++hb)
-        acc[vb][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[vb], fb[hb], acc[vb][hb], 0, 0, 0);
+  auto mf = [&](const Frag& f, int i) {  // MFMA i of a 16-state step: block (i / 4, i % 4)
+    const int vb = i >> 2, hb = i & 3;
+    const bf16x8 fa = __builtin_bit_cast(bf16x8, __builtin_shufflevector(f.lo[vb], f.hi[vb], 0, 1, 2, 3, 4, 5, 6, 7));
+    acc[vb][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, f.b[hb], acc[vb][hb], 0, 0, 0);
   };
 
   // ---- accumulators start at the tile's bias; words >= V at -inf
@@ -235,17 +284,19 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
 
   // ---- epilogue state
   float st_m[4], st_s[4];  // running (max, sum of exp(x - max)) of the lane's rows
-  float lval[KC];          // owner (row = tid): sorted k best of the split so far
-  int lidx[KC];
+  // owner (row = tid): the k best (score, word) of the split so far as
+  // descending 64-bit keys; the first KC - k slots hold sentinels above any key
+  uint64_t lkey[KC];
   float published = kNoThr;
 #pragma unroll
   for (int hb = 0; hb < 4; ++hb) {
     st_m[hb] = kStatInit;
     st_s[hb] = 0.f;
   }
-  list_init<KC>(lval, lidx, k);
+#pragma unroll
+  for (int j = 0; j < KC; ++j) lkey[j] = (j < KC - k) ? ~0ull : 0ull;
   ep.thr[tid] = kNoThr;
-  ep.cnt[tid] = 0;
+  ep.cnt[tid] = 0u;
   if (tid < 4) ep.flag[tid] = 0;
 
   auto publish = [&](float v) {
@@ -292,17 +343,15 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
     }
 
     // first tile of the split: seed each row's threshold.  Every holder finds
-    // the j-th largest of its 16 quad maxima (j = ceil(k / 4)); the row then
-    // has at least 4 j >= k distinct scores >= the smallest of the four.
+    // the 4 largest of its 16 quad maxima; these 16 distinct scores of the row
+    // are gathered and their k-th largest (k <= 16) is a valid threshold: k
+    // scores of the row are >= it.
     if (vt == vt0) {
-      const int jj = (k + 3) >> 2;
 #pragma unroll
       for (int hb = 0; hb < 4; ++hb) {
 #pragma unroll
         for (int vb = 0; vb < 4; ++vb) opaque(acc[vb][hb]);
-        float sv[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) sv[j] = (j < 4 - jj) ? INFINITY : -INFINITY;
+        float sv[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
 #pragma unroll
         for (int vb = 0; vb < 4; ++vb)
 #pragma unroll
@@ -315,12 +364,27 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
               sv[j] = hi;
             }
           }
-        ep.u.red[wh * 128 + hb * 32 + col][holder] = sv[3];
+        *reinterpret_cast<float4*>(&ep.u.red[wh * 128 + hb * 32 + col][4 * holder]) =
+            make_float4(sv[0], sv[1], sv[2], sv[3]);
         done(sv[3]);
       }
       lds_barrier();
       {
-        const float seed = fminf(fminf(ep.u.red[tid][0], ep.u.red[tid][1]), fminf(ep.u.red[tid][2], ep.u.red[tid][3]));
+        // k-th largest of the 16: right-aligned list of KC slots, +inf sentinels first
+        float kv[KC];
+#pragma unroll
+        for (int j = 0; j < KC; ++j) kv[j] = (j < KC - k) ? INFINITY : -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          float x = ep.u.red[tid][i];
+#pragma unroll
+          for (int j = 0; j < KC; ++j) {
+            const float hi = fmaxf(kv[j], x);
+            x = fminf(kv[j], x);
+            kv[j] = hi;
+          }
+        }
+        const float seed = kv[KC - 1];
         if (seed > ep.thr[tid]) {
           ep.thr[tid] = seed;
           publish(seed);
@@ -329,9 +393,11 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
       lds_barrier();
     }
 
-    // candidate rounds: a lane appends, in position order, every score >= the
-    // row's threshold; if the row's list is full it stops at that position and
-    // resumes there in the next round, against the raised threshold
+    // candidate rounds.  A lane appends, in position order, every score >= the
+    // row's threshold to its own CAPH slots of the row; past CAPH it notes the
+    // first position it could not append and resumes there in the next round,
+    // against the raised threshold.  Quads are skipped unless some lane of the
+    // wave needs them, and appends use masked stores, not branches.
     int resume[4];
 #pragma unroll
     for (int hb = 0; hb < 4; ++hb) {
@@ -343,36 +409,42 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
       int ovf = 0;
 #pragma unroll
       for (int hb = 0; hb < 4; ++hb) {
-        if (resume[hb] < G::DONE) {
-#pragma unroll
-          for (int vb = 0; vb < 4; ++vb) opaque(acc[vb][hb]);
+        const int rs = resume[hb];
+        if (__builtin_amdgcn_ballot_w64(rs < G::DONE) != 0ull) {
           const int rl = wh * 128 + hb * 32 + col;
           const float t = fmaxf(ep.thr[rl], key2f(ep.tgk[par][rl]));
-          const int rs = resume[hb];
-          // word of position (vb, q, j) = wbase + 32 vb + 8 q + j; opaque so that
-          // the 64 words are formed on demand, not hoisted out of the loop
-          int wbase = v0 + wv * 128 + 4 * half;
-          asm volatile("" : "+v"(wbase));
-          int newres = G::DONE;
+          int newres = G::DONE, c = 0;
+          // the lane's slots of the row (LDS byte addresses, opaque so that the
+          // per-slot addresses are formed at the store, not kept in registers)
+          uint32_t sx = lds_addr(&ep.u.c.x[rl][holder][0]), sp = lds_addr(&ep.u.c.p[rl][holder][0]);
+          asm volatile("" : "+v"(sx), "+v"(sp));
 #pragma unroll
-          for (int vb = 0; vb < 4; ++vb)
+          for (int vb = 0; vb < 4; ++vb) {
+            opaque(acc[vb][hb]);  // only this block's 16 scores in VGPRs at a time
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-              if (max4(acc[vb][hb], q) >= t && vb * 16 + 4 * q + 3 >= rs && newres == G::DONE) {
+              const bool qp = max4(acc[vb][hb], q) >= t && vb * 16 + 4 * q + 3 >= rs;
+              if (__builtin_amdgcn_ballot_w64(qp) != 0ull) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                   const int pos = vb * 16 + 4 * q + j;
                   const float x = acc[vb][hb][4 * q + j];
-                  if (x >= t && pos >= rs && newres == G::DONE) {
-                    const int slot = atomicAdd(&ep.cnt[rl], 1);
-                    if (slot < G::CAP)
-                      ep.u.cand[rl][slot] = make_int2(__float_as_int(x), wbase + vb * 32 + 8 * q + j);
-                    else
-                      newres = pos;
+                  const bool pred = x >= t && pos >= rs;
+                  const bool room = c < G::CAPH;
+                  newres = (pred && !room) ? min(newres, pos) : newres;
+                  if (pred && room) {
+                    int pv = pos;  // materialized here, not hoisted (64 constants would pin VGPRs)
+                    asm volatile("" : "+v"(pv));
+                    *(KB_LDS float*)(uintptr_t)(sx + 4 * c) = x;
+                    *(KB_LDS uint8_t*)(uintptr_t)(sp + c) = (uint8_t)pv;
                   }
+                  c += (pred && room) ? 1 : 0;
                 }
               }
             }
+            done(c);
+          }
+          reinterpret_cast<uint8_t*>(&ep.cnt[rl])[holder] = (uint8_t)c;
           resume[hb] = newres;
           ovf |= newres != G::DONE;
           done(newres);
@@ -382,16 +454,33 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
       lds_barrier();
       if (tid == 0) ep.flag[(round + 1) & 1] = 0;  // read only after the next barrier
       {
-        const int c = min(ep.cnt[tid], G::CAP);
-        for (int i = 0; i < c; ++i) {
-          const int2 e = ep.u.cand[tid][i];
-          const float cv = __int_as_float(e.x);
-          if (better(cv, e.y, lval[KC - 1], lidx[KC - 1])) list_insert<KC>(lval, lidx, cv, e.y);
+        const uint32_t cw = ep.cnt[tid];
+        if (cw != 0u) {
+#pragma unroll
+          for (int hd = 0; hd < 4; ++hd) {
+            const int c = (cw >> (8 * hd)) & 0xFF;
+            // word of position p of holder hd: holder = 2 wv + half
+            const int wb = v0 + (hd >> 1) * 128 + (hd & 1) * 4;
+            for (int i = 0; i < c; ++i) {
+              const int p = ep.u.c.p[tid][hd][i];
+              const int word = wb + (p >> 4) * 32 + ((p >> 2) & 3) * 8 + (p & 3);
+              uint64_t key = cand_key(ep.u.c.x[tid][hd][i], word);
+              if (key > lkey[KC - 1]) {
+#pragma unroll
+                for (int j = 0; j < KC; ++j) {
+                  const uint64_t hi = key > lkey[j] ? key : lkey[j];
+                  key = key > lkey[j] ? lkey[j] : key;
+                  lkey[j] = hi;
+                }
+              }
+            }
+          }
+          ep.cnt[tid] = 0u;
         }
-        ep.cnt[tid] = 0;
-        if (lval[KC - 1] > ep.thr[tid]) {
-          ep.thr[tid] = lval[KC - 1];
-          publish(lval[KC - 1]);
+        const float kth = key2f((uint32_t)(lkey[KC - 1] >> 32));
+        if (kth > ep.thr[tid]) {
+          ep.thr[tid] = kth;
+          publish(kth);
         }
       }
       lds_barrier();
@@ -401,12 +490,12 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
 
   // ---- the stage pipeline
   uint16_t* const bufs[4] = {S0, S1, S2, S3};
-  bf16x8 fa0[4], fb0[4], fa1[4], fb1[4];
+  Frag F0, F1;
 
-  issue_next(S0);
-  issue_next(S1);
-  issue_next(S2);
-  issue_next(S3);
+  issue_whole(S0);
+  issue_whole(S1);
+  issue_whole(S2);
+  issue_whole(S3);
   // stage 0 landed: at most the three later stages outstanding
   if (total >= 4)
     wait_vm<3 * G::OPS>();
@@ -418,17 +507,32 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
     wait_vm<0>();
   lds_barrier();
   init_acc(vt0);
-  load_frags(S0, 0, fa0, fb0);
+#pragma unroll
+  for (int u = 0; u < 12; ++u) rd(S0, 0, u, F0);
 
+  // One stage (32 states) on buffer b.  LDS reads (two per MFMA, early, so
+  // they have landed before their use) and DMA instructions (one per MFMA)
+  // sit between MFMAs, where their issue hides behind the MFMA pipe:
+  //   16 MFMAs on F0 (first 16 states), reading F1 (second 16) in between;
+  //   wait for stage g + 1, barrier (buffer b is free everywhere);
+  //   16 MFMAs on F1, reading F0 of stage g + 1 and issuing stage g + 4 into b.
   int g = 0;
-  auto body = [&](auto bc) {
+  auto body = [&](auto bc, auto rc) {
     constexpr int b = decltype(bc)::value;
+    constexpr bool read_next = decltype(rc)::value;  // false in a tile's last stage: the next
+                                                     // tile's first fragments are read after
+                                                     // the epilogue (keeps VGPRs free for it)
     uint16_t* const cur = bufs[b];
     uint16_t* const nxt = bufs[(b + 1) & 3];
-    load_frags(cur, 1, fa1, fb1);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma16(fa0, fb0);
-    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      mf(F0, i);
+      if (i < 6) {
+        rd(cur, 1, 2 * i, F1);
+        rd(cur, 1, 2 * i + 1, F1);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
     if (g + 1 < total) {
       const int ahead = total - 2 - g;  // stages issued after g + 1
       if (ahead >= 2)
@@ -438,24 +542,54 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
       else
         wait_vm<0>();
       lds_barrier();  // stage g + 1 landed everywhere; every wave is done with buffer b
-      issue_next(cur);
-      load_frags(nxt, 0, fa0, fb0);
+    } else {
+      wait_vm<0>();  // the last stage: the shared-threshold keys of the last tile
+      lds_barrier();
     }
     __builtin_amdgcn_sched_barrier(0);
-    mfma16(fa1, fb1);
-    __builtin_amdgcn_sched_barrier(0);
+    const bool more = issued < total;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      mf(F1, i);
+      if (read_next && i < 6) {  // (stale but in-bounds after the last stage)
+        rd(nxt, 0, 2 * i, F0);
+        rd(nxt, 0, 2 * i + 1, F0);
+      }
+      if (more && i >= G::DMA_SLOT0 && i < G::DMA_SLOT0 + 8) dma_part(cur, i - G::DMA_SLOT0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (more) dma_finish();
+    // the shared thresholds for this tile's epilogue, read three stages before
+    // its end, when every split has published its previous tile: the wait for
+    // stage g + 1 of the tile's last stage covers this load (it is issued
+    // before the DMA of the stages that wait leaves outstanding)
+    if (wave == 1 && ((g + 4) % nk) == 0) dma16(a.gthr + h0 + lane * 4, lds_addr(&ep.tgk[(g / nk) & 1][0]));
     ++g;
   };
 
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  using RD = std::true_type;
+  using NR = std::false_type;
   for (int vt = vt0; vt < vt1; ++vt) {
-    for (int kt = 0; kt < nk; kt += 4) {
-      body(std::integral_constant<int, 0>{});
-      body(std::integral_constant<int, 1>{});
-      body(std::integral_constant<int, 2>{});
-      body(std::integral_constant<int, 3>{});
+    for (int kt = 0; kt < nk - 4; kt += 4) {
+      body(I0{}, RD{});
+      body(I1{}, RD{});
+      body(I2{}, RD{});
+      body(I3{}, RD{});
     }
+    body(I0{}, RD{});
+    body(I1{}, RD{});
+    body(I2{}, RD{});
+    body(I3{}, NR{});
     epilogue(vt);
-    if (vt + 1 < vt1) init_acc(vt + 1);
+    if (vt + 1 < vt1) {
+      init_acc(vt + 1);
+#pragma unroll
+      for (int u = 0; u < 12; ++u) rd(S0, 0, u, F0);  // the next tile starts on buffer 0
+    }
   }
 
   // ---- this split's partial of every row: merge the four holders' statistics
@@ -477,7 +611,9 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
     a.stats[row] = make_float2(M, S);
 #pragma unroll
     for (int j = 0; j < KC; ++j)
-      if (j >= KC - k) a.lists[row * k + (j - (KC - k))] = make_int2(__float_as_int(lval[j]), lidx[j]);
+      if (j >= KC - k)
+        a.lists[row * k + (j - (KC - k))] =
+            make_int2(__float_as_int(key2f((uint32_t)(lkey[j] >> 32))), (int)~(uint32_t)lkey[j]);
   }
 }
 

@@ -43,7 +43,9 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 // compiler does not insert its own (conservative) waits for it; callers wait
 // with s_waitcnt vmcnt before reading the data.  One wait state after M0.
 __device__ __forceinline__ void dma16(const void* g, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_base) : "m0");
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g),
+               "s"(__builtin_amdgcn_readfirstlane(lds_base))
+               : "m0");
 }
 
 // ---------------------------------------------------------------- K1
