@@ -37,8 +37,8 @@ if ROOT not in sys.path:
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 K1_SOURCES = [os.path.join(ROOT, "paper_1805_09863_amd", "csrc", f)
-              for f in ("kb_common.hpp", "k1_common.hpp", "k1_dma.hpp", "k1_fused.hpp")]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k1_cfg3_hbm_traffic.txt")
+              for f in ("kb_common.hpp", "k1_common.hpp", "k1_wide.hpp")]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k1_wide_N3072_H1024_V90000_k12_hbm_traffic.txt")
 
 
 def log(msg: str):
@@ -71,11 +71,15 @@ class HipEvents:
 
 
 def k1_source_hash() -> str:
-    """Hash of the projection kernel's sources: counter summaries apply only to this code."""
+    """Hash of the projection kernel's code (line comments and blank lines
+    dropped): counter summaries apply only to this code."""
     h = hashlib.sha256()
     for p in K1_SOURCES:
-        with open(p, "rb") as f:
-            h.update(f.read())
+        with open(p) as f:
+            for line in f:
+                code = line.split("//", 1)[0].rstrip()
+                if code:
+                    h.update(code.encode() + b"\n")
     return h.hexdigest()[:16]
 
 
@@ -160,7 +164,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--cpu-sample-sentences", type=int, default=64)
+    ap.add_argument("--cpu-sample-sentences", type=int, default=160)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode-loop", action="store_true")
     ap.add_argument("--print-k1-hash", action="store_true", help="print the projection-kernel source hash and exit")
@@ -195,9 +199,8 @@ def main():
         print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "launches": 3}))
         return
     kb.lib()
-    cfg_i = 3
     log("generating the V=90k workload ...")
-    inp = wl.make_config(cfg_i)
+    inp = wl.make_workload(wl.V90K)
     N, H, V, k, S = inp.N, inp.H, inp.V, inp.k, inp.S
     h, W, b, prev, off = to_dev(inp, torch, np)
     tok = torch.empty((S, k), dtype=torch.int32, device="cuda")
@@ -243,7 +246,7 @@ def main():
                    "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": read_traffic(),
-                     "kernel": "k1_dma (projection + bias + softmax statistics + per-split k-best)",
+                     "kernel": "k1_wide (projection + bias + softmax statistics + per-split k-best)",
                      "kernel_ms": k1_mean, "flops_per_launch": flops},
     }
     tr = result["roofline"]["traffic"]

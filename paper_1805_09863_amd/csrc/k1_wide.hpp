@@ -15,11 +15,13 @@
 // V-contiguous (A-fragments via the LDS transpose read), h rows are
 // row-major 64-byte slices per stage.
 //
-// Per stage the wave reads the second half of its fragments, runs the first
-// half's 16 MFMAs, waits for the next stage and passes the only barrier of
-// the stage, refills the buffer it just finished with the stage four ahead,
-// reads the next stage's first fragments and runs the second half's MFMAs.
-// LDS reads therefore always overlap MFMAs, and no wait drains the ring.
+// Per stage the wave runs the first half's 16 MFMAs while it reads the
+// second half's fragments and issues the W rows of the stage three ahead
+// (into the buffer every wave finished before the previous barrier), waits
+// for the next stage and passes the only barrier of the stage, then runs the
+// second half's MFMAs while it reads the next stage's first fragments and
+// issues the h rows of the stage three ahead.  LDS reads and DMA issue
+// therefore always overlap MFMAs, and no wait drains the ring.
 //
 // Epilogue per tile (the accumulators start at the bias, so Algorithm 3's
 // AddBias costs nothing; words >= V start at -inf and drop out everywhere):
@@ -44,7 +46,7 @@ struct WideGeom {
   static constexpr int WE = BK * BV;  // bf16 elements of W per stage
   static constexpr int HE = BH * BK;  // bf16 elements of h per stage
   static constexpr int OPS = 8;       // DMA instructions per wave per stage
-  static constexpr int DMA_SLOT0 = 6; // first MFMA (of a stage's second 16) followed by a DMA instruction
+  static constexpr int DMA_SLOT0 = 8; // first MFMA (of each 16) followed by a DMA instruction
   static constexpr int CAPH = 5;      // candidate slots per row and holder per round
   static constexpr int DONE = 64;     // "no pending candidates" position
 };
@@ -412,7 +414,8 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
         const int rs = resume[hb];
         if (__builtin_amdgcn_ballot_w64(rs < G::DONE) != 0ull) {
           const int rl = wh * 128 + hb * 32 + col;
-          const float t = fmaxf(ep.thr[rl], key2f(ep.tgk[par][rl]));
+          // lanes with nothing pending on this row compare against +inf
+          const float t = rs < G::DONE ? fmaxf(ep.thr[rl], key2f(ep.tgk[par][rl])) : INFINITY;
           int newres = G::DONE, c = 0;
           // the lane's slots of the row (LDS byte addresses, opaque so that the
           // per-slot addresses are formed at the store, not kept in registers)
@@ -424,7 +427,7 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
               const bool qp = max4(acc[vb][hb], q) >= t && vb * 16 + 4 * q + 3 >= rs;
-              if (__builtin_amdgcn_ballot_w64(qp) != 0ull) {
+              if (__builtin_amdgcn_ballot_w64(qp) != 0ull) {  // a uniform skip for most quads
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                   const int pos = vb * 16 + 4 * q + j;
@@ -466,12 +469,14 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
               const int word = wb + (p >> 4) * 32 + ((p >> 2) & 3) * 8 + (p & 3);
               uint64_t key = cand_key(ep.u.c.x[tid][hd][i], word);
               if (key > lkey[KC - 1]) {
+                // insertion with independent compares: the keys are descending,
+                // so gt[] is false then true; the key lands at the first true
+                bool gt[KC];
 #pragma unroll
-                for (int j = 0; j < KC; ++j) {
-                  const uint64_t hi = key > lkey[j] ? key : lkey[j];
-                  key = key > lkey[j] ? lkey[j] : key;
-                  lkey[j] = hi;
-                }
+                for (int j = 0; j < KC; ++j) gt[j] = key > lkey[j];
+#pragma unroll
+                for (int j = KC - 1; j > 0; --j) lkey[j] = gt[j] ? (gt[j - 1] ? lkey[j - 1] : key) : lkey[j];
+                lkey[0] = gt[0] ? key : lkey[0];
               }
             }
           }
@@ -492,14 +497,13 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
   uint16_t* const bufs[4] = {S0, S1, S2, S3};
   Frag F0, F1;
 
+  // three stages ahead: stage g + 3 goes into the buffer of stage g - 1,
+  // which every wave finished reading before the barrier of stage g - 1
   issue_whole(S0);
   issue_whole(S1);
   issue_whole(S2);
-  issue_whole(S3);
-  // stage 0 landed: at most the three later stages outstanding
-  if (total >= 4)
-    wait_vm<3 * G::OPS>();
-  else if (total == 3)
+  // stage 0 landed: at most the two later stages outstanding
+  if (total >= 3)
     wait_vm<2 * G::OPS>();
   else if (total == 2)
     wait_vm<G::OPS>();
@@ -511,11 +515,14 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
   for (int u = 0; u < 12; ++u) rd(S0, 0, u, F0);
 
   // One stage (32 states) on buffer b.  LDS reads (two per MFMA, early, so
-  // they have landed before their use) and DMA instructions (one per MFMA)
-  // sit between MFMAs, where their issue hides behind the MFMA pipe:
-  //   16 MFMAs on F0 (first 16 states), reading F1 (second 16) in between;
-  //   wait for stage g + 1, barrier (buffer b is free everywhere);
-  //   16 MFMAs on F1, reading F0 of stage g + 1 and issuing stage g + 4 into b.
+  // they have landed before their use) and DMA instructions (one per MFMA,
+  // spread over the whole stage so the address unit is never flooded) sit
+  // between MFMAs, where their issue hides behind the MFMA pipe:
+  //   16 MFMAs on F0 (first 16 states), reading F1 (second 16) and issuing
+  //   the W rows of stage g + 3 into buffer b - 1;
+  //   wait for stage g + 1, barrier;
+  //   16 MFMAs on F1, reading F0 of stage g + 1 and issuing the h rows of
+  //   stage g + 3.
   int g = 0;
   auto body = [&](auto bc, auto rc) {
     constexpr int b = decltype(bc)::value;
@@ -524,6 +531,8 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
                                                      // the epilogue (keeps VGPRs free for it)
     uint16_t* const cur = bufs[b];
     uint16_t* const nxt = bufs[(b + 1) & 3];
+    uint16_t* const fill = bufs[(b + 3) & 3];
+    const bool more = issued < total;  // stage g + 3 exists
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       mf(F0, i);
@@ -531,23 +540,24 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
         rd(cur, 1, 2 * i, F1);
         rd(cur, 1, 2 * i + 1, F1);
       }
+      if (more && i >= G::DMA_SLOT0 && i < G::DMA_SLOT0 + 4) dma_part(fill, i - G::DMA_SLOT0);
       __builtin_amdgcn_sched_barrier(0);
     }
     if (g + 1 < total) {
-      const int ahead = total - 2 - g;  // stages issued after g + 1
-      if (ahead >= 2)
-        wait_vm<2 * G::OPS>();
-      else if (ahead == 1)
+      // DMA instructions issued after stage g + 1's: stage g + 2 (whole) and
+      // the W half of stage g + 3
+      if (g + 3 < total)
+        wait_vm<G::OPS + G::OPS / 2>();
+      else if (g + 2 < total)
         wait_vm<G::OPS>();
       else
         wait_vm<0>();
-      lds_barrier();  // stage g + 1 landed everywhere; every wave is done with buffer b
+      lds_barrier();  // stage g + 1 landed everywhere
     } else {
       wait_vm<0>();  // the last stage: the shared-threshold keys of the last tile
       lds_barrier();
     }
     __builtin_amdgcn_sched_barrier(0);
-    const bool more = issued < total;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       mf(F1, i);
@@ -555,7 +565,7 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
         rd(nxt, 0, 2 * i, F0);
         rd(nxt, 0, 2 * i + 1, F0);
       }
-      if (more && i >= G::DMA_SLOT0 && i < G::DMA_SLOT0 + 8) dma_part(cur, i - G::DMA_SLOT0);
+      if (more && i >= G::DMA_SLOT0 && i < G::DMA_SLOT0 + 4) dma_part(fill, 4 + i - G::DMA_SLOT0);
       __builtin_amdgcn_sched_barrier(0);
     }
     if (more) dma_finish();

@@ -79,13 +79,15 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // Rows from which the 256 x 256 tile pays off (it needs the DMA pipeline).
 constexpr int kWideMinRows = 513;
+// The wide kernel's W source offsets assume at least one full 256-word tile.
+constexpr int kWideMinCols = 256;
 
 // Shapes the DMA pipeline accepts, pointer alignment aside.
 bool dma_shape(int dtype, int H, int V) { return dtype == KB_BF16 && H % 128 == 0 && V % 8 == 0; }
 
 Plan make_plan(int dtype, int N, int H, int V, int k, bool dma) {
   Plan p{};
-  if (dma && N >= kWideMinRows && dma_shape(dtype, H, V)) {
+  if (dma && N >= kWideMinRows && V >= kWideMinCols && dma_shape(dtype, H, V)) {
     p.layout = kb::K1_W256;
     p.BH = 256;
     p.BV = 256;

@@ -2,6 +2,7 @@
 
 Holds random draws and data layout only, never the method's arithmetic.
 """
-from .workloads import (CONFIGS, SEED_BASE, LoopWorkload, StepInputs, add_near_ties,  # noqa: F401
-                        bf16_bits_to_f32, config_seed, f32_to_bf16_bits, make_config,
-                        make_loop_workload, make_step, uniform_offsets)
+from .workloads import (LOOP, NEARTIE, SEED_BASE, SMALL, V60K, V90K, WORKLOADS,  # noqa: F401
+                        LoopWorkload, StepInputs, add_near_ties, bf16_bits_to_f32, f32_to_bf16_bits,
+                        make_loop_workload, make_step, make_workload, uniform_offsets, workload_index,
+                        workload_seed)

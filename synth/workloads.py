@@ -169,37 +169,49 @@ def add_near_ties(inp: StepInputs, frac: float = 0.01, delta: float = 1e-6,
 
 
 # --------------------------------------------------------------------------
-# the five workloads
+# the five workloads (sizes in the names)
 # --------------------------------------------------------------------------
-CONFIGS = [
-    dict(name="cfg0_S1_beam5_H256_V8000_k5_f32", S=1, beam=5, H=256, V=8000, k=5, dtype="f32"),
-    dict(name="cfg1_S64_beam5_H512_V30000_k5_f32_neartie", S=64, beam=5, H=512, V=30000, k=5, dtype="f32"),
-    dict(name="cfg2_S128_beam5_H1024_V60000_k5_bf16", S=128, beam=5, H=1024, V=60000, k=5, dtype="bf16"),
-    dict(name="cfg3_S256_beam12_H1024_V90000_k12_bf16_zipf", S=256, beam=12, H=1024, V=90000, k=12,
-         dtype="bf16"),
-    dict(name="cfg4_loop_S512_beam5_H1024_V50000_k5_bf16", S=512, beam=5, H=1024, V=50000, k=5,
+WORKLOADS = [
+    dict(name="S1_beam5_H256_V8000_k5_f32", S=1, beam=5, H=256, V=8000, k=5, dtype="f32"),
+    dict(name="S64_beam5_H512_V30000_k5_f32_neartie", S=64, beam=5, H=512, V=30000, k=5, dtype="f32",
+         near_ties=True),
+    dict(name="S128_beam5_H1024_V60000_k5_bf16", S=128, beam=5, H=1024, V=60000, k=5, dtype="bf16"),
+    dict(name="S256_beam12_H1024_V90000_k12_bf16_zipf", S=256, beam=12, H=1024, V=90000, k=12,
+         dtype="bf16", bias="zipf"),
+    dict(name="loop_S512_beam5_H1024_V50000_k5_bf16", S=512, beam=5, H=1024, V=50000, k=5,
          dtype="bf16", T=60, Lmin=5, Lmax=60),
 ]
+SMALL = WORKLOADS[0]["name"]
+NEARTIE = WORKLOADS[1]["name"]
+V60K = WORKLOADS[2]["name"]
+V90K = WORKLOADS[3]["name"]
+LOOP = WORKLOADS[4]["name"]
 
 
-def config_seed(i: int) -> int:
-    return SEED_BASE + i
+def workload_index(name: str) -> int:
+    for i, c in enumerate(WORKLOADS):
+        if c["name"] == name:
+            return i
+    raise KeyError(f"no workload named {name!r}")
 
 
-def make_config(i: int, seed: Optional[int] = None) -> StepInputs:
-    """Single-step inputs of workload ``i`` (0-3), or the first step of workload 4."""
-    c = CONFIGS[i]
-    sd = config_seed(i) if seed is None else seed
-    bias = "zipf" if i == 3 else "uniform"
+def workload_seed(name: str) -> int:
+    return SEED_BASE + workload_index(name)
+
+
+def make_workload(name: str, seed: Optional[int] = None) -> StepInputs:
+    """Single-step inputs of a named workload (for the decode-loop workload, its first step)."""
+    c = WORKLOADS[workload_index(name)]
+    sd = workload_seed(name) if seed is None else seed
     inp = make_step(H=c["H"], V=c["V"], k=c["k"], S=c["S"], beam=c["beam"], dtype=c["dtype"],
-                    seed=sd, bias=bias, name=c["name"])
-    if i == 1:
+                    seed=sd, bias=c.get("bias", "uniform"), name=c["name"])
+    if c.get("near_ties"):
         inp = add_near_ties(inp, frac=0.01, delta=1e-6, seed=sd + 1000)
     return inp
 
 
 # --------------------------------------------------------------------------
-# workload 4: multi-step decode schedule
+# the decode-loop workload: multi-step decode schedule
 # --------------------------------------------------------------------------
 @dataclasses.dataclass
 class LoopWorkload:
@@ -241,9 +253,9 @@ class LoopWorkload:
 def make_loop_workload(seed: Optional[int] = None, S: Optional[int] = None, V: Optional[int] = None,
                        H: Optional[int] = None, T: Optional[int] = None,
                        Lmin: Optional[int] = None, Lmax: Optional[int] = None) -> LoopWorkload:
-    """Workload 4 (optionally shrunk for tests): lengths, weights, bias, step-0 scores."""
-    c = CONFIGS[4]
-    sd = config_seed(4) if seed is None else seed
+    """The decode-loop workload (optionally shrunk for tests): lengths, weights, bias, step-0 scores."""
+    c = WORKLOADS[workload_index(LOOP)]
+    sd = workload_seed(LOOP) if seed is None else seed
     S = c["S"] if S is None else S
     V = c["V"] if V is None else V
     H = c["H"] if H is None else H

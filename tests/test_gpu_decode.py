@@ -99,5 +99,5 @@ def test_decode_loop_small(kb):
 
 def test_decode_loop_config4(kb):
     work = wl.make_loop_workload()
-    say(f"config 4 loop: S={work.S} V={work.V} H={work.H} T={work.T}")
+    say(f"decode-loop workload: S={work.S} V={work.V} H={work.H} T={work.T}")
     _run(kb, work, sample_per_step=2)

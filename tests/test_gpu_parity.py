@@ -62,6 +62,7 @@ WIDE = [
     ([4] * 256, 1024, 30000, 4),               # four whole row tiles
     ([3] * 250 + [2] * 20, 256, 6216, 8),      # mixed beams, N 790
     ([6] * 100, 128, 1024, 6),                 # 4 word tiles: one tile per split
+    ([5] * 120, 128, 200, 5),                  # V < 256: planned on the 256 x 128 tile
 ]
 
 
@@ -125,18 +126,18 @@ def test_duplicate_rows_lower_parent_wins(kb):
             seen.add((p, t))
 
 
-@pytest.mark.parametrize("cfg", [0, 1, 2])
-def test_config_full(kb, cfg):
-    inp = wl.make_config(cfg)
-    say(f"config {cfg}: {inp.name} N={inp.N}")
+@pytest.mark.parametrize("name", [wl.SMALL, wl.NEARTIE, wl.V60K])
+def test_config_full(kb, name):
+    inp = wl.make_workload(name)
+    say(f"workload {inp.name} N={inp.N}")
     out = run_step(kb, inp, row_lse=True)
     rep, _ = check(inp, out)
     say(f"  max score err {rep.max_score_err:.2e}, {rep.n_checked_idx} exact ranks")
 
 
-def test_config3_sampled(kb):
-    inp = wl.make_config(3)
-    say(f"config 3: {inp.name} N={inp.N}, oracle on sampled sentences")
+def test_config_v90k_sampled(kb):
+    inp = wl.make_workload(wl.V90K)
+    say(f"workload {inp.name} N={inp.N}, oracle on sampled sentences")
     out = run_step(kb, inp, row_lse=True)
     sents = sorted(set(np.random.default_rng(3).choice(inp.S, 12, replace=False).tolist()) | {0, inp.S - 1})
     rep, _ = check(inp, out, sentences=sents)

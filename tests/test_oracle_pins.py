@@ -291,10 +291,10 @@ def test_threshold_shortcut_equals_full_sort_random_and_ties():
         assert np.array_equal(a.score, c.score) and np.array_equal(a.next_score, c.next_score)
 
 
-@pytest.mark.parametrize("cfg", [0, 1])
-def test_threshold_shortcut_equals_full_sort_configs(cfg):
-    inp = wl.make_config(cfg)
-    if cfg == 1:        # a sample of sentences keeps the CPU suite short
+@pytest.mark.parametrize("name", [wl.SMALL, wl.NEARTIE])
+def test_threshold_shortcut_equals_full_sort_configs(name):
+    inp = wl.make_workload(name)
+    if name == wl.NEARTIE:        # a sample of sentences keeps the CPU suite short
         inp = _slice_sentences(inp, range(0, 64, 8))
     a = ko.kbest_step(inp.h, inp.W, inp.b, inp.prev, inp.off, inp.k, inp.dtype)
     c = ko.kbest_step_threshold(inp.h, inp.W, inp.b, inp.prev, inp.off, inp.k, inp.dtype)
