@@ -124,10 +124,12 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
   int row_tile, split;
   k1_cell(a, blockIdx.x, row_tile, split);
   const int h0 = row_tile * BH;
-  const int vt0 = split * a.tps;
-  const int vt1 = min(vt0 + a.tps, a.n_vtiles);
+  // the split's tiles are split, split + P, split + 2P, ...: interleaved, so
+  // every split meets the high-scoring words of a skewed bias (low word ids
+  // under a Zipf-like prior) early and no split is left with all of them
+  const int nt = (a.n_vtiles - split + a.P - 1) / a.P;
   const int nk = a.H / BK;  // a multiple of 4: every tile starts on ring buffer 0
-  const int total = (vt1 - vt0) * nk;
+  const int total = nt * nk;
 
   // ---- per-lane DMA byte offsets (fixed for the whole kernel)
   // W slot s = 256 wave + 64 i + lane: stage row r = s / 32, physical chunk
@@ -148,7 +150,7 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
   // wsrc / hsrc point at its first W row / h column; wdma are the W offsets of
   // its tile (clamped for the last, ragged tile: words >= V read word V - 8..
   // instead, which start at -inf).
-  int iv0 = vt0 * BV, ik0 = 0, it = 0, issued = 0;
+  int iv0 = split * BV, ik0 = 0, it = 0, issued = 0;
   const char* wsrc = reinterpret_cast<const char*>(a.W) + (size_t)iv0 * 2;
   const char* hsrc = reinterpret_cast<const char*>(a.h);
   uint32_t wdma[4];
@@ -188,7 +190,7 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
     hsrc += BK * 2;
     if (ik0 == a.H) {
       ik0 = 0;
-      iv0 += BV;
+      iv0 += a.P * BV;
       ++it;
       wsrc = reinterpret_cast<const char*>(a.W) + (size_t)iv0 * 2;
       hsrc = reinterpret_cast<const char*>(a.h);
@@ -253,9 +255,9 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
   };
 
   // ---- accumulators start at the tile's bias; words >= V at -inf
-  auto init_acc = [&](int vt) {
-    const int par = (vt - vt0) & 1;
-    const int v0 = vt * BV;
+  auto init_acc = [&](int ti) {  // ti: the tile's ordinal within the split
+    const int par = ti & 1;
+    const int v0 = (split + ti * a.P) * BV;
     const bool ragged = v0 + BV > a.V;
     // word of (vb, i, j) is valid iff vb * 32 + 8 i + j < lim
     const int lim = a.V - v0 - wv * 128 - 4 * half;
@@ -308,9 +310,9 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
     }
   };
 
-  auto epilogue = [&](int vt) {
-    const int par = (vt - vt0) & 1;
-    const int v0 = vt * BV;
+  auto epilogue = [&](int ti) {
+    const int par = ti & 1;
+    const int v0 = (split + ti * a.P) * BV;
     float tmax[4];
     // statistics (Algorithm 4, one rescale per tile)
 #pragma unroll
@@ -348,7 +350,7 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
     // the 4 largest of its 16 quad maxima; these 16 distinct scores of the row
     // are gathered and their k-th largest (k <= 16) is a valid threshold: k
     // scores of the row are >= it.
-    if (vt == vt0) {
+    if (ti == 0) {
 #pragma unroll
       for (int hb = 0; hb < 4; ++hb) {
 #pragma unroll
@@ -510,7 +512,7 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
   else
     wait_vm<0>();
   lds_barrier();
-  init_acc(vt0);
+  init_acc(0);
 #pragma unroll
   for (int u = 0; u < 12; ++u) rd(S0, 0, u, F0);
 
@@ -583,7 +585,7 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
   using I3 = std::integral_constant<int, 3>;
   using RD = std::true_type;
   using NR = std::false_type;
-  for (int vt = vt0; vt < vt1; ++vt) {
+  for (int ti = 0; ti < nt; ++ti) {
     for (int kt = 0; kt < nk - 4; kt += 4) {
       body(I0{}, RD{});
       body(I1{}, RD{});
@@ -594,9 +596,9 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
     body(I1{}, RD{});
     body(I2{}, RD{});
     body(I3{}, NR{});
-    epilogue(vt);
-    if (vt + 1 < vt1) {
-      init_acc(vt + 1);
+    epilogue(ti);
+    if (ti + 1 < nt) {
+      init_acc(ti + 1);
 #pragma unroll
       for (int u = 0; u < 12; ++u) rd(S0, 0, u, F0);  // the next tile starts on buffer 0
     }
