@@ -49,6 +49,7 @@ struct WideGeom {
   static constexpr int DMA_SLOT0 = 8; // first MFMA (of each 16) followed by a DMA instruction
   static constexpr int CAPH = 5;      // candidate slots per row and holder per round
   static constexpr int DONE = 64;     // "no pending candidates" position
+  static constexpr int MS = 16;       // splits that share their running row maxima
 };
 
 struct alignas(16) WideEpi {
@@ -101,6 +102,25 @@ __device__ __forceinline__ void done(int x) { asm volatile("" ::"v"(x)); }
 // that equal scores compare equal.
 __device__ __forceinline__ uint64_t cand_key(float x, int word) {
   return ((uint64_t)f2key(x + 0.0f) << 32) | (uint32_t)~(uint32_t)word;
+}
+
+// Global atomic max and 16-byte load issued from inline assembly: the
+// compiler then adds no waits of its own for them (its conservative
+// vmcnt(0) would also wait for the DMA stages in flight).  The atomic's
+// completion is never waited for; the load is waited for with load_wait.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void atomic_umax_nowait(uint32_t* p, uint32_t v) {
+  asm volatile("global_atomic_umax %0, %1, off" ::"v"(p), "v"(v) : "memory");
+}
+__device__ __forceinline__ u32x4 load16_async(const void* p) {
+  u32x4 v;
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(p));
+  return v;
+}
+// every vector memory operation of the wave done; the registers pass
+// through so that their uses stay behind the wait
+__device__ __forceinline__ void load_wait(u32x4& a, u32x4& b, u32x4& c, u32x4& d) {
+  asm volatile("s_waitcnt vmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d));
 }
 
 __device__ __forceinline__ float max4(const f32x16& x, int q) {
@@ -305,7 +325,7 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
 
   auto publish = [&](float v) {
     if (h0 + tid < a.N && v > published) {
-      atomicMax(&a.gthr[h0 + tid], f2key(v));
+      atomic_umax_nowait(&a.gthr[h0 + tid], f2key(v));
       published = v;
     }
   };
@@ -313,7 +333,18 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
   auto epilogue = [&](int ti) {
     const int par = ti & 1;
     const int v0 = (split + ti * a.P) * BV;
+    // the running maxima splits 0..MS-1 have shared for the owner's row
+    // (loaded now, used after the statistics)
+    // (k > 12: the longer k-list leaves no registers for them; not used)
+    constexpr bool kShare = KC <= 12;
+    u32x4 gm[4];
+    if (kShare && ti > 0) {
+      const uint32_t* gp = a.gmax + (size_t)(h0 + tid) * G::MS;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) gm[i] = load16_async(gp + 4 * i);
+    }
     float tmax[4];
+    bool grew[4];
     // statistics (Algorithm 4, one rescale per tile)
 #pragma unroll
     for (int hb = 0; hb < 4; ++hb) {
@@ -331,6 +362,7 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
       const float mx = fmaxf(m0, m1);
       tmax[hb] = mx;
       const float mnew = fmaxf(st_m[hb], mx);
+      grew[hb] = mx > st_m[hb];
       const float ml2 = mnew * kL2E;
       float s0 = st_s[hb] * exp2_fast((st_m[hb] - mnew) * kL2E), s1 = 0.f;
 #pragma unroll
@@ -344,6 +376,50 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
       st_m[hb] = mnew;
       done(st_s[hb]);
       done(mx);
+    }
+    if (kShare && ti > 0) {
+      // the k-th largest of the shared maxima: they are scores of k distinct
+      // words of the row, so it is a lower bound of the row's k-th best.  It
+      // is worked out only where at least k of them beat the row's present
+      // threshold (else it cannot raise it): insertion into a right-aligned
+      // descending list by median-of-three.
+      load_wait(gm[0], gm[1], gm[2], gm[3]);  // long landed: issued before the statistics
+      uint32_t key[G::MS];
+#pragma unroll
+      for (int i = 0; i < G::MS / 4; ++i) {
+        key[4 * i] = gm[i].x;
+        key[4 * i + 1] = gm[i].y;
+        key[4 * i + 2] = gm[i].z;
+        key[4 * i + 3] = gm[i].w;
+      }
+      const uint32_t tk = max(f2key(ep.thr[tid]), ep.tgk[par][tid]);
+      int above = 0;
+#pragma unroll
+      for (int i = 0; i < G::MS; ++i) above += key[i] > tk ? 1 : 0;
+      if (__builtin_amdgcn_ballot_w64(above >= k) != 0ull) {
+        float kv[KC];
+#pragma unroll
+        for (int j = 0; j < KC; ++j) kv[j] = (j < KC - k) ? INFINITY : -INFINITY;
+#pragma unroll
+        for (int i = 0; i < G::MS; ++i) {
+          const float x = key2f(key[i]);
+#pragma unroll
+          for (int j = KC - 1; j > 0; --j) kv[j] = __builtin_amdgcn_fmed3f(kv[j - 1], kv[j], x);
+          kv[0] = fmaxf(kv[0], x);
+        }
+        const float t2 = kv[KC - 1];
+        if (above >= k && t2 > ep.thr[tid]) {
+          ep.thr[tid] = t2;
+          publish(t2);
+        }
+      }
+      lds_barrier();  // the holders read the raised threshold below
+    }
+    // share the holder's running max (the row's is the max of the four)
+    if (kShare && split < G::MS) {
+#pragma unroll
+      for (int hb = 0; hb < 4; ++hb)
+        if (grew[hb]) atomic_umax_nowait(&a.gmax[(size_t)(h0 + wh * 128 + hb * 32 + col) * G::MS + split], f2key(st_m[hb]));
     }
 
     // first tile of the split: seed each row's threshold.  Every holder finds

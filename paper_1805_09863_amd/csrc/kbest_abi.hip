@@ -72,10 +72,13 @@ constexpr int kTargetCUs = 256;
 struct Plan {
   int layout, kc, BH, BV;
   int row_tiles, n_vtiles, P, tps;
-  size_t stats_off, lists_off, gthr_off, bytes;
+  size_t stats_off, lists_off, gthr_off, gmax_off, bytes;
 };
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Splits whose running row maxima the 256 x 256 tile kernel shares (16 keys per row).
+constexpr int kGmaxSplits = 16;
 
 // Rows from which the 256 x 256 tile pays off (it needs the DMA pipeline).
 constexpr int kWideMinRows = 513;
@@ -116,7 +119,9 @@ Plan make_plan(int dtype, int N, int H, int V, int k, bool dma) {
   p.stats_off = 0;
   p.lists_off = align_up((size_t)p.P * N * sizeof(float2), 256);
   p.gthr_off = align_up(p.lists_off + (size_t)p.P * N * k * sizeof(int2), 256);
-  p.bytes = align_up(p.gthr_off + (size_t)p.row_tiles * p.BH * sizeof(uint32_t), 256);
+  p.gmax_off = p.gthr_off + (size_t)p.row_tiles * p.BH * sizeof(uint32_t);  // right after gthr: one reset
+  const size_t gmax_n = p.layout == kb::K1_W256 ? (size_t)p.row_tiles * p.BH * kGmaxSplits : 0;
+  p.bytes = align_up(p.gmax_off + gmax_n * sizeof(uint32_t), 256);
   return p;
 }
 
@@ -177,12 +182,14 @@ int kbest_step_impl(int dtype, int N, int H, int V, int k, int S, const void* h,
   a1.stats = reinterpret_cast<float2*>((char*)ws + p.stats_off);
   a1.lists = reinterpret_cast<int2*>((char*)ws + p.lists_off);
   a1.gthr = reinterpret_cast<uint32_t*>((char*)ws + p.gthr_off);
+  a1.gmax = reinterpret_cast<uint32_t*>((char*)ws + p.gmax_off);
   a1.row_tiles = p.row_tiles;
   a1.P = p.P;
   a1.grp = p.row_tiles < 4 ? p.row_tiles : 4;
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
 
-  hipError_t e = kb::launch_zero_u32(a1.gthr, p.row_tiles * p.BH, hs);
+  const int n_zero = p.row_tiles * p.BH * (p.layout == kb::K1_W256 ? 1 + kGmaxSplits : 1);  // gthr (+ gmax)
+  hipError_t e = kb::launch_zero_u32(a1.gthr, n_zero, hs);
   if (e != hipSuccess) return fail(KB_ERR_HIP, "threshold reset kernel launch: %s", hipGetErrorString(e));
 
   if (ev0) {
