@@ -1,0 +1,55 @@
+/*
+ * kbest_standin.h -- decoder stand-in of the synthetic decode loop.
+ *
+ * Not part of the output layer.  The paper's decoder (an RNN) produces the
+ * state h of every live hypothesis before each output-layer step; the loop
+ * that measures mini-batching (Section 2.1, Algorithm 2 against the constant
+ * batch of Algorithm 1) replaces it by a seeded table of states and a drawn
+ * length per sentence, at which all of the sentence's continuations end.
+ * These two calls keep that bookkeeping on the device, so a loop step needs
+ * no host work beyond reading two counts.  Conventions (caller-owned device
+ * buffers, stream ordering, kb_status returns, kb_last_error) are those of
+ * kbest.h; the functions live in the same library.
+ */
+#ifndef KBEST_STANDIN_H
+#define KBEST_STANDIN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/*
+ * kb_standin_alive -- alive[s*k + r] = (t < lengths[sid[s]] - 1) ? 1 : 0 for
+ * s < S, r < k: the batch entries that stay after step t, when sentence s
+ * (original id sid[s]) emits EOS on every continuation at step
+ * lengths[sid[s]] - 1.
+ *   sid      S int32, original sentence ids (indices into lengths).
+ *   lengths  int32 per original sentence.
+ *   alive    S*k uint8 output, the input of kb_compact_batch.
+ * S == 0 is a no-op.  0 <= S, 1 <= k, S*k fits in int32.
+ */
+int kb_standin_alive(int S, int k, int t, const int32_t* sid, const int32_t* lengths, uint8_t* alive,
+                     void* stream);
+
+/*
+ * kb_standin_next_h -- the states of step t for the entries kept by
+ * kb_compact_batch: for i < n = min(n_max, *n_dev) (n_max if n_dev is NULL),
+ *   e = keep[i];  out[i, :] = table[(sid[e / k] * T + t) * k + e % k, :]
+ * i.e. the table row of (original sentence sid[e / k], step t, beam slot
+ * e % k); rows are row_bytes long (a positive multiple of 4).
+ *   keep     kb_compact_batch's keep_idx (entries of the old S x k batch).
+ *   sid      the OLD batch's original sentence ids (S_old int32).
+ *   table    (S0 * T * k) rows; out at least n_max rows.  4-byte aligned.
+ * 0 <= t < T; keep and sid must index valid entries (not checked).
+ */
+int kb_standin_next_h(int n_max, const int32_t* n_dev, int k, int T, int t, const int32_t* keep,
+                      const int32_t* sid, const void* table, void* out, size_t row_bytes, void* stream);
+
+#ifdef __cplusplus
+} /* extern "C" */
+#endif
+
+#endif /* KBEST_STANDIN_H */

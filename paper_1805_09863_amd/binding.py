@@ -25,7 +25,7 @@ _P = ctypes.c_void_p
 _I = ctypes.c_int
 _SZ = ctypes.c_size_t
 
-# name -> (restype, argtypes), mirroring include/kbest.h
+# name -> (restype, argtypes), mirroring include/kbest.h and include/kbest_standin.h
 SIGNATURES = {
     "kb_abi_version": (_I, []),
     "kb_status_string": (ctypes.c_char_p, [_I]),
@@ -36,6 +36,9 @@ SIGNATURES = {
                                   _P, _P]),
     "kb_compact_batch": (_I, [_I, _I, _P, _P, _P, _P, _P, _P, _P]),
     "kb_gather_rows": (_I, [_I, _P, _P, _P, _P, _SZ, _P]),
+    # decoder stand-in of the synthetic decode loop (include/kbest_standin.h)
+    "kb_standin_alive": (_I, [_I, _I, _I, _P, _P, _P, _P]),
+    "kb_standin_next_h": (_I, [_I, _P, _I, _I, _I, _P, _P, _P, _P, _SZ, _P]),
 }
 
 
@@ -194,4 +197,21 @@ def gather_rows(src: torch.Tensor, idx: torch.Tensor, *, n_dev: Optional[torch.T
         return out
     _check(lib().kb_gather_rows(n_max, _ptr(n_dev), _ptr(idx), _ptr(src), _ptr(out), row_bytes,
                                 _stream(stream)))
+    return out
+
+
+# ---------------------------------------------------------------- decoder stand-in
+def standin_alive(sid: torch.Tensor, lengths: torch.Tensor, S: int, k: int, t: int, *, out: torch.Tensor,
+                  stream=None) -> torch.Tensor:
+    """out[s*k + r] = (t < lengths[sid[s]] - 1) for s < S (include/kbest_standin.h)."""
+    _check(lib().kb_standin_alive(S, k, t, _ptr(sid), _ptr(lengths), _ptr(out), _stream(stream)))
+    return out
+
+
+def standin_next_h(table: torch.Tensor, keep: torch.Tensor, sid: torch.Tensor, k: int, T: int, t: int,
+                   n_max: int, *, n_dev: Optional[torch.Tensor] = None, out: torch.Tensor, stream=None):
+    """out[i] = table[(sid[keep[i] // k] * T + t) * k + keep[i] % k] for i < min(n_max, n_dev[0])."""
+    row_bytes = table[0].numel() * table.element_size()
+    _check(lib().kb_standin_next_h(n_max, _ptr(n_dev), k, T, t, _ptr(keep), _ptr(sid), _ptr(table), _ptr(out),
+                                   row_bytes, _stream(stream)))
     return out

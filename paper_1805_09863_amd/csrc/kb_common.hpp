@@ -118,4 +118,11 @@ hipError_t launch_compact(int S, int k, const uint8_t* alive, int32_t* keep, int
 hipError_t launch_gather(int n_max, const int32_t* n_dev, const int32_t* idx, const void* src,
                          void* dst, size_t row_bytes, hipStream_t st);
 
+// ---------------------------------------------------------------- decoder stand-in
+hipError_t launch_standin_alive(int S, int k, int t, const int32_t* sid, const int32_t* lengths, uint8_t* alive,
+                                hipStream_t st);
+hipError_t launch_standin_next_h(int n_max, const int32_t* n_dev, int k, int T, int t, const int32_t* keep,
+                                 const int32_t* sid, const void* table, void* out, size_t row_bytes,
+                                 hipStream_t st);
+
 }  // namespace kb

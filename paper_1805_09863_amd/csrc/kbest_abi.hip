@@ -7,6 +7,7 @@
 #include <string>
 
 #include "kbest.h"
+#include "kbest_standin.h"
 #include "kb_common.hpp"
 
 namespace kb {
@@ -285,6 +286,32 @@ int kb_gather_rows(int n_max, const int32_t* n_dev, const int32_t* idx, const vo
   if (!aligned(src, 4) || !aligned(dst, 4)) return fail(KB_ERR_INVALID_ARG, "src and dst must be 4-byte aligned");
   hipError_t e = kb::launch_gather(n_max, n_dev, idx, src, dst, row_bytes, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(KB_ERR_HIP, "gather kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int kb_standin_alive(int S, int k, int t, const int32_t* sid, const int32_t* lengths, uint8_t* alive,
+                     void* stream) {
+  if (S < 0 || k < 1) return fail(KB_ERR_INVALID_ARG, "S = %d, k = %d", S, k);
+  if ((long long)S * k > INT_MAX) return fail(KB_ERR_UNSUPPORTED, "S*k does not fit in int32");
+  if (S == 0) return ok();
+  if (!sid || !lengths || !alive) return fail(KB_ERR_INVALID_ARG, "null sid, lengths or alive");
+  hipError_t e = kb::launch_standin_alive(S, k, t, sid, lengths, alive, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "stand-in alive kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int kb_standin_next_h(int n_max, const int32_t* n_dev, int k, int T, int t, const int32_t* keep, const int32_t* sid,
+                      const void* table, void* out, size_t row_bytes, void* stream) {
+  if (n_max < 0 || k < 1 || T < 1 || t < 0 || t >= T)
+    return fail(KB_ERR_INVALID_ARG, "n_max = %d, k = %d, T = %d, t = %d", n_max, k, T, t);
+  if (row_bytes == 0 || row_bytes % 4 != 0) return fail(KB_ERR_INVALID_ARG, "row_bytes must be a positive multiple of 4");
+  if (row_bytes / 4 > INT_MAX) return fail(KB_ERR_UNSUPPORTED, "row too long");
+  if (n_max == 0) return ok();
+  if (!keep || !sid || !table || !out) return fail(KB_ERR_INVALID_ARG, "null keep, sid, table or out");
+  if (!aligned(table, 4) || !aligned(out, 4)) return fail(KB_ERR_INVALID_ARG, "table and out must be 4-byte aligned");
+  hipError_t e = kb::launch_standin_next_h(n_max, n_dev, k, T, t, keep, sid, table, out, row_bytes,
+                                           reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "stand-in state gather launch: %s", hipGetErrorString(e));
   return ok();
 }
 

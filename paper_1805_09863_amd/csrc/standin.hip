@@ -1,0 +1,65 @@
+// Decoder stand-in of the synthetic decode loop.  Not part of the output
+// layer: the method leaves the decoder (an RNN in the paper) outside the
+// step, and the loop that measures mini-batching (Section 2.1, Algorithm 2)
+// replaces it by a seeded table of states and a drawn length per sentence.
+// These kernels keep that bookkeeping on the device so that a loop step
+// costs a handful of launches:
+//   * standin_alive: entry s*k + r of the batch stays unless its sentence
+//     reaches its drawn length this step (every continuation ends together);
+//   * standin_next_h: the next step's state of each surviving entry, read
+//     from the table at (original sentence id, step, beam slot).
+#include "kb_common.hpp"
+
+namespace kb {
+
+__global__ __launch_bounds__(256) void standin_alive(int S, int k, int t, const int32_t* __restrict__ sid,
+                                                     const int32_t* __restrict__ lengths,
+                                                     uint8_t* __restrict__ alive) {
+  const int n = S * k;
+  for (int e = blockIdx.x * 256 + threadIdx.x; e < n; e += gridDim.x * 256)
+    alive[e] = t < lengths[sid[e / k]] - 1 ? 1 : 0;
+}
+
+template <class V>
+__global__ __launch_bounds__(256) void standin_next_h(int n_max, const int32_t* __restrict__ n_dev, int k, int T,
+                                                      int t, const int32_t* __restrict__ keep,
+                                                      const int32_t* __restrict__ sid, const V* __restrict__ table,
+                                                      V* __restrict__ out, int row_words) {
+  const int n = n_dev ? min(n_max, *n_dev) : n_max;
+  const long long total = (long long)n * row_words;
+  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < total; i += (long long)gridDim.x * 256) {
+    const int r = (int)(i / row_words);
+    const int w = (int)(i - (long long)r * row_words);
+    const int e = keep[r];
+    const long long src = ((long long)sid[e / k] * T + t) * k + e % k;
+    out[i] = table[src * row_words + w];
+  }
+}
+
+hipError_t launch_standin_alive(int S, int k, int t, const int32_t* sid, const int32_t* lengths, uint8_t* alive,
+                                hipStream_t st) {
+  const int n = S * k;
+  const int blocks = n > 0 ? min((n + 255) / 256, 1024) : 1;
+  standin_alive<<<dim3(blocks), dim3(256), 0, st>>>(S, k, t, sid, lengths, alive);
+  return hipGetLastError();
+}
+
+hipError_t launch_standin_next_h(int n_max, const int32_t* n_dev, int k, int T, int t, const int32_t* keep,
+                                 const int32_t* sid, const void* table, void* out, size_t row_bytes,
+                                 hipStream_t st) {
+  const bool v16 = (row_bytes % 16 == 0) && ((uintptr_t)table % 16 == 0) && ((uintptr_t)out % 16 == 0);
+  const size_t words = v16 ? row_bytes / 16 : row_bytes / 4;
+  const long long total = (long long)n_max * (long long)words;
+  int blocks = (int)((total + 255) / 256);
+  blocks = blocks < 1 ? 1 : (blocks > 8192 ? 8192 : blocks);
+  if (v16)
+    standin_next_h<uint4><<<dim3(blocks), dim3(256), 0, st>>>(n_max, n_dev, k, T, t, keep, sid,
+                                                              (const uint4*)table, (uint4*)out, (int)words);
+  else
+    standin_next_h<uint32_t><<<dim3(blocks), dim3(256), 0, st>>>(n_max, n_dev, k, T, t, keep, sid,
+                                                                 (const uint32_t*)table, (uint32_t*)out,
+                                                                 (int)words);
+  return hipGetLastError();
+}
+
+}  // namespace kb

@@ -6,8 +6,8 @@ The decoder RNN is not part of this library: each row's state h for step t
 comes from a device table indexed by (sentence, step, beam slot), standing in
 for the decoder.  Every output-layer step (projection, fused softmax/k-best,
 beam merge) and every compaction and state gather runs in libkbest's kernels;
-the few small torch ops here only form the decoder stand-in's row indices and
-the EOS mask of the schedule.
+the decoder stand-in's bookkeeping (EOS mask of the schedule, next states)
+runs in its own small kernels (include/kbest_standin.h).
 """
 from __future__ import annotations
 
@@ -26,10 +26,6 @@ class LoopStats:
     total_rows: int = 0
 
 
-def _hrow_index(sid_rows: torch.Tensor, slot_rows: torch.Tensor, t: int, T: int, beam: int) -> torch.Tensor:
-    return ((sid_rows.long() * T + t) * beam + slot_rows.long()).to(torch.int32)
-
-
 def decode_loop(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, lengths: torch.Tensor,
                 prev0: torch.Tensor, k: int, T: int, *, compact: bool = True,
                 on_step: Optional[Callable] = None, stream=None) -> LoopStats:
@@ -37,13 +33,20 @@ def decode_loop(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, lengths
 
     ``h_table`` is (S0*T*beam) x H on the device (row (s*T + t)*beam + r is the
     state of slot r of sentence s at step t), ``lengths`` S0 int32: sentence s
-    emits EOS on all its continuations at step L_s - 1.  ``prev0`` holds the
-    S0*k scores of the step-0 hypotheses (beam = k rows per sentence).
+    emits EOS on all its continuations at step L_s - 1 (1 <= L_s <= T).
+    ``prev0`` holds the S0*k scores of the step-0 hypotheses (beam = k rows
+    per sentence).
 
     ``compact=True``: after each step the finished entries are removed
     (Algorithm 2) and the loop ends when the batch is empty.
     ``compact=False``: the batch keeps all S0 sentences until the longest is
     done (Algorithm 1); finished sentences' rows are decoded and ignored.
+
+    A compacted step enqueues the output layer, the stand-in's EOS mask, the
+    compaction, the gathers of the surviving scores and sentence ids and the
+    stand-in's next states, then waits for the two counts (rows, sentences)
+    that size the next step's launch: one host synchronisation per step,
+    after all of the step's work is queued.
 
     ``on_step(t, state)`` is called after each output-layer step with a dict
     of the device tensors of that step.
@@ -51,45 +54,80 @@ def decode_loop(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, lengths
     dev = W.device
     beam = k
     S0 = lengths.numel()
-    Lmax = int(lengths.max().item()) if S0 > 0 else 0
-    sid = torch.arange(S0, dtype=torch.int32, device=dev)            # original id of each live sentence
-    row_sid = sid.repeat_interleave(beam)
-    row_slot = torch.arange(beam, dtype=torch.int32, device=dev).repeat(S0)
-    prev = prev0.to(torch.float32).contiguous()
-    off = (torch.arange(S0 + 1, dtype=torch.int32, device=dev) * beam).contiguous()
-    S, N = S0, S0 * beam
     H, V = W.shape
+    stats = LoopStats()
+    if S0 == 0:
+        return stats
+    len_host = lengths.cpu().tolist()
+    Lmax = max(len_host)
+    if Lmax > T or min(len_host) < 1:
+        raise ValueError("lengths must lie in [1, T]")
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    M0 = S0 * k
+    lengths = lengths.to(device=dev, dtype=torch.int32).contiguous()
     # the plan (and so the workspace) depends on the row count, which shrinks
     dt = kbb._dtype_code(W)
-    ws = kbb.workspace(max(kbb.kbest_workspace_bytes(dt, s * beam, H, V, k, s) for s in range(1, S0 + 1))
-                       if S0 > 0 else 1, dev)
-    h_cur = torch.empty((N, H), dtype=h_table.dtype, device=dev)
-    stats = LoopStats()
-    len_host = lengths.cpu().tolist()
-    lengths = lengths.to(device=dev, dtype=torch.int32)
-    t = 0
-    while (S > 0) if compact else (t < Lmax):
-        hidx = _hrow_index(row_sid, row_slot, t, T, beam)
-        kbb.gather_rows(h_table, hidx, out=h_cur[:N], stream=stream)
-        tok, par, sc = kbb.kbest_step(h_cur[:N], W, b, prev, off, k, S=S, ws=ws, stream=stream)
-        stats.rows.append(N if compact else sum(1 for L in len_host if L > t) * beam)
-        if on_step is not None:
-            on_step(t, dict(h=h_cur[:N], prev=prev, off=off, sid=sid, token=tok, parent=par, score=sc, S=S, N=N))
-        if compact:
-            alive = (t < lengths[sid.long()] - 1).to(torch.uint8).repeat_interleave(k)
-            keep, kept, noff, ksent, nS = kbb.compact_batch(alive, S, k, stream=stream)
-            n_new, s_new = (int(x) for x in torch.cat([kept, nS]).cpu())   # the step's one host sync
-            prev = kbb.gather_rows(sc.view(S * k, 1), keep, n_max=n_new, stream=stream).view(n_new)
-            new_sid = kbb.gather_rows(sid.view(S, 1), ksent, n_max=s_new, stream=stream).view(s_new)
-            kk = keep[:n_new].long()
-            row_sid = sid[kk // k] if n_new else sid[:0]
-            row_slot = (kk % k).to(torch.int32)
-            sid, S, N = new_sid, s_new, n_new
-            off = noff[:s_new + 1].contiguous()
-        else:
-            prev = sc.view(S * k)
-            row_slot = torch.arange(beam, dtype=torch.int32, device=dev).repeat(S0)
-        t += 1
+    ws = kbb.workspace(max(kbb.kbest_workspace_bytes(dt, s * beam, H, V, k, s) for s in range(1, S0 + 1)), dev)
+    i32 = dict(dtype=torch.int32, device=dev)
+    tok = torch.empty(M0, **i32)
+    par = torch.empty(M0, **i32)
+    sc = torch.empty(M0, dtype=torch.float32, device=dev)
+    h_cur = torch.empty((M0, H), dtype=h_table.dtype, device=dev)
+    ident = torch.arange(M0, **i32)                      # entry e of an S0 x k batch is row e
+    sid = torch.arange(S0, **i32)                        # original id of each live sentence
+    off = (torch.arange(S0 + 1, **i32) * beam).contiguous()
+    prev = prev0.to(torch.float32).contiguous()
+    kbb.standin_next_h(h_table, ident, sid, k, T, 0, M0, out=h_cur, stream=stream)
+    S, N, t = S0, M0, 0
+    if compact:
+        alive = torch.empty(M0, dtype=torch.uint8, device=dev)
+        keep = torch.empty(M0, **i32)
+        cnt = torch.empty(2, **i32)                      # kept rows, kept sentences
+        noff = torch.empty(S0 + 1, **i32)
+        ksent = torch.empty(S0, **i32)
+        prev_nx = torch.empty(M0, dtype=torch.float32, device=dev)
+        sid_nx = torch.empty(S0, **i32)
+        cnt_host = torch.empty(2, dtype=torch.int32, pin_memory=True)
+        ready = torch.cuda.Event()
+        while S > 0:
+            kbb.kbest_step(h_cur[:N], W, b, prev[:N], off[:S + 1], k, S=S,
+                           out=(tok[:S * k].view(S, k), par[:S * k].view(S, k), sc[:S * k].view(S, k)),
+                           ws=ws, stream=stream)
+            stats.rows.append(N)
+            if on_step is not None:
+                on_step(t, dict(h=h_cur[:N], prev=prev[:N], off=off[:S + 1], sid=sid[:S],
+                                token=tok[:S * k].view(S, k), parent=par[:S * k].view(S, k),
+                                score=sc[:S * k].view(S, k), S=S, N=N))
+            kbb.standin_alive(sid, lengths, S, k, t, out=alive, stream=stream)
+            kbb.compact_batch(alive[:S * k], S, k, out=(keep, cnt[0:1], noff, ksent, cnt[1:2]), stream=stream)
+            cnt_host.copy_(cnt, non_blocking=True)
+            ready.record(stream)
+            kbb.gather_rows(sc[:S * k].view(S * k, 1), keep, n_dev=cnt[0:1], n_max=S * k,
+                            out=prev_nx.view(M0, 1), stream=stream)
+            kbb.gather_rows(sid[:S].view(S, 1), ksent, n_dev=cnt[1:2], n_max=S, out=sid_nx.view(S0, 1),
+                            stream=stream)
+            if t + 1 < T:
+                kbb.standin_next_h(h_table, keep, sid, k, T, t + 1, S * k, n_dev=cnt[0:1], out=h_cur,
+                                   stream=stream)
+            ready.synchronize()                            # the step's one host sync
+            N, S = (int(x) for x in cnt_host.tolist())
+            prev, prev_nx = prev_nx, prev
+            sid, sid_nx = sid_nx, sid
+            off, noff = noff, off
+            t += 1
+    else:
+        while t < Lmax:
+            kbb.kbest_step(h_cur, W, b, prev, off, k, S=S0,
+                           out=(tok.view(S0, k), par.view(S0, k), sc.view(S0, k)), ws=ws, stream=stream)
+            stats.rows.append(sum(1 for L in len_host if L > t) * beam)
+            if on_step is not None:
+                on_step(t, dict(h=h_cur, prev=prev, off=off, sid=sid, token=tok.view(S0, k),
+                                parent=par.view(S0, k), score=sc.view(S0, k), S=S0, N=M0))
+            prev, sc = sc, prev                            # this step's scores feed the next
+            if t + 1 < T:
+                kbb.standin_next_h(h_table, ident, sid, k, T, t + 1, M0, out=h_cur, stream=stream)
+            t += 1
     stats.steps = t
     stats.total_rows = sum(stats.rows)
     return stats

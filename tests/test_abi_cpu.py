@@ -3,6 +3,7 @@
 Every call here returns before any HIP work is enqueued, so no GPU is needed.
 """
 import ctypes
+import glob
 import os
 import re
 
@@ -16,19 +17,38 @@ FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: validation fails first
 
 
 def _header_functions(repo_root):
-    with open(os.path.join(repo_root, "include", "kbest.h")) as f:
-        text = f.read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(kb_[a-z0-9_]+)\s*\(", text)))
+    names = set()
+    for h in sorted(glob.glob(os.path.join(repo_root, "include", "*.h"))):
+        with open(h) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names |= set(re.findall(r"\b(kb_[a-z0-9_]+)\s*\(", text))
+    return sorted(names)
 
 
 def test_library_exports_every_declared_function(repo_root):
     L = binding.lib()
     names = _header_functions(repo_root)
-    assert len(names) >= 8
+    assert len(names) >= 10
     for n in names:
-        assert hasattr(L, n), f"{n} declared in kbest.h but not exported"
-    assert set(names) == set(binding.SIGNATURES), "binding signatures out of sync with kbest.h"
+        assert hasattr(L, n), f"{n} declared in include/*.h but not exported"
+    assert set(names) == set(binding.SIGNATURES), "binding signatures out of sync with include/*.h"
+
+
+def test_standin_argument_checks():
+    L = binding.lib()
+    assert L.kb_standin_alive(0, 5, 0, None, None, None, None) == KB_OK            # empty batch: no-op
+    assert L.kb_standin_alive(-1, 5, 0, FAKE, FAKE, FAKE, None) == KB_ERR_INVALID_ARG
+    assert L.kb_standin_alive(3, 0, 0, FAKE, FAKE, FAKE, None) == KB_ERR_INVALID_ARG
+    assert L.kb_standin_alive(3, 5, 0, None, FAKE, FAKE, None) == KB_ERR_INVALID_ARG
+    assert L.kb_standin_alive(1 << 30, 4, 0, FAKE, FAKE, FAKE, None) == KB_ERR_UNSUPPORTED
+    nh = L.kb_standin_next_h
+    assert nh(0, None, 5, 60, 1, FAKE, FAKE, FAKE, FAKE, 2048, None) == KB_OK        # nothing to gather
+    assert nh(4, None, 5, 60, 60, FAKE, FAKE, FAKE, FAKE, 2048, None) == KB_ERR_INVALID_ARG   # t >= T
+    assert nh(4, None, 5, 60, -1, FAKE, FAKE, FAKE, FAKE, 2048, None) == KB_ERR_INVALID_ARG
+    assert nh(4, None, 5, 60, 1, FAKE, FAKE, FAKE, FAKE, 6, None) == KB_ERR_INVALID_ARG       # row bytes % 4
+    assert nh(4, None, 5, 60, 1, None, FAKE, FAKE, FAKE, 2048, None) == KB_ERR_INVALID_ARG
+    assert nh(4, None, 5, 60, 1, FAKE, FAKE, ctypes.c_void_p(0x1002), FAKE, 2048, None) == KB_ERR_INVALID_ARG
 
 
 def test_abi_version_and_status_strings():
