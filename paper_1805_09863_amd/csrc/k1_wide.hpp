@@ -312,6 +312,7 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
   // descending 64-bit keys; the first KC - k slots hold sentinels above any key
   uint64_t lkey[KC];
   float published = kNoThr;
+  float rowbest = kNoThr, shared_best = kNoThr;  // best listed score of the row, and the one shared
 #pragma unroll
   for (int hb = 0; hb < 4; ++hb) {
     st_m[hb] = kStatInit;
@@ -330,13 +331,14 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
     }
   };
 
+  // splits 0..MS-1 share their best row scores (k > 12: the longer k-list
+  // leaves no registers for the maxima; not used)
+  constexpr bool kShare = KC <= 12;
   auto epilogue = [&](int ti) {
     const int par = ti & 1;
     const int v0 = (split + ti * a.P) * BV;
     // the running maxima splits 0..MS-1 have shared for the owner's row
     // (loaded now, used after the statistics)
-    // (k > 12: the longer k-list leaves no registers for them; not used)
-    constexpr bool kShare = KC <= 12;
     u32x4 gm[4];
     if (kShare && ti > 0) {
       const uint32_t* gp = a.gmax + (size_t)(h0 + tid) * G::MS;
@@ -344,7 +346,6 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
       for (int i = 0; i < 4; ++i) gm[i] = load16_async(gp + 4 * i);
     }
     float tmax[4];
-    bool grew[4];
     // statistics (Algorithm 4, one rescale per tile)
 #pragma unroll
     for (int hb = 0; hb < 4; ++hb) {
@@ -362,7 +363,6 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
       const float mx = fmaxf(m0, m1);
       tmax[hb] = mx;
       const float mnew = fmaxf(st_m[hb], mx);
-      grew[hb] = mx > st_m[hb];
       const float ml2 = mnew * kL2E;
       float s0 = st_s[hb] * exp2_fast((st_m[hb] - mnew) * kL2E), s1 = 0.f;
 #pragma unroll
@@ -410,16 +410,9 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
         const float t2 = kv[KC - 1];
         if (above >= k && t2 > ep.thr[tid]) {
           ep.thr[tid] = t2;
-          publish(t2);
         }
       }
       lds_barrier();  // the holders read the raised threshold below
-    }
-    // share the holder's running max (the row's is the max of the four)
-    if (kShare && split < G::MS) {
-#pragma unroll
-      for (int hb = 0; hb < 4; ++hb)
-        if (grew[hb]) atomic_umax_nowait(&a.gmax[(size_t)(h0 + wh * 128 + hb * 32 + col) * G::MS + split], f2key(st_m[hb]));
     }
 
     // first tile of the split: seed each row's threshold.  Every holder finds
@@ -467,7 +460,6 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
         const float seed = kv[KC - 1];
         if (seed > ep.thr[tid]) {
           ep.thr[tid] = seed;
-          publish(seed);
         }
       }
       lds_barrier();
@@ -547,6 +539,7 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
               const int word = wb + (p >> 4) * 32 + ((p >> 2) & 3) * 8 + (p & 3);
               uint64_t key = cand_key(ep.u.c.x[tid][hd][i], word);
               if (key > lkey[KC - 1]) {
+                rowbest = fmaxf(rowbest, ep.u.c.x[tid][hd][i]);
                 // insertion with independent compares: the keys are descending,
                 // so gt[] is false then true; the key lands at the first true
                 bool gt[KC];
@@ -561,13 +554,20 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
           ep.cnt[tid] = 0u;
         }
         const float kth = key2f((uint32_t)(lkey[KC - 1] >> 32));
-        if (kth > ep.thr[tid]) {
-          ep.thr[tid] = kth;
-          publish(kth);
-        }
+        if (kth > ep.thr[tid]) ep.thr[tid] = kth;
       }
       lds_barrier();
       if (ep.flag[round & 1] == 0) break;
+    }
+    // shared on the split's tiles 0, 1, 2, 4, 8, ... only (device-wide
+    // atomics are written through to memory; a stale value is still a valid
+    // bound): the row's threshold, and the best score of the row this split
+    // has listed (its maximum, unless that never reached a threshold; any
+    // score of the split is a valid entry of the shared maxima)
+    if ((ti & (ti - 1)) == 0) publish(ep.thr[tid]);
+    if (kShare && split < G::MS && (ti & (ti - 1)) == 0 && rowbest > shared_best && h0 + tid < a.N) {
+      atomic_umax_nowait(&a.gmax[(size_t)(h0 + tid) * G::MS + split], f2key(rowbest));
+      shared_best = rowbest;
     }
   };
 
