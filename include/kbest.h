@@ -136,6 +136,27 @@ int kb_kbest_step_events(int dtype, int N, int H, int V, int k, int S,
                          void* proj_begin_event, void* proj_end_event);
 
 /*
+ * kb_argmax_step -- greedy decoding (beam 1): the best word of every row,
+ * without any softmax (Algorithm 5: argmax of p = W h + b; Algorithm 6: the
+ * vocabulary is sharded, each shard's (max, best) found in parallel, then
+ * reduced).
+ *   h, W, b           as for kb_kbest_step (N rows; no sentences, no prev).
+ *   out_token         N int32: argmax_j (h[n] . W[:, j] + b[j]); among equal
+ *                     maxima the lowest j (the strict '>' scans of the paper).
+ *   out_logit         N float32: that maximum, h[n] . W[:, j] + b[j] (a raw
+ *                     score, not a probability).
+ *   workspace         at least kb_argmax_workspace_bytes(dtype, N, H, V)
+ *                     bytes, 256-byte aligned, caller-owned scratch.
+ * N == 0 is a no-op.  1 <= H, 1 <= V.  Errors and alignment as for
+ * kb_kbest_step.  Scores accumulate in float32 (bf16 products are exact), so
+ * words whose scores differ by less than the accumulation error may swap.
+ */
+size_t kb_argmax_workspace_bytes(int dtype, int N, int H, int V);
+int kb_argmax_step(int dtype, int N, int H, int V, const void* h, const void* W, const float* b,
+                   int32_t* out_token, float* out_logit, void* workspace, size_t workspace_bytes,
+                   void* stream);
+
+/*
  * kb_compact_batch -- remove finished hypotheses from the batch (Section 2.1,
  * Algorithm 2: after each Decode, every hypothesis that produced EOS leaves
  * the batch; decoding stops when the batch is empty).

@@ -272,6 +272,36 @@ def argmax_sharded(p, b, n_shards: int) -> int:
     return best
 
 
+@dataclass
+class ArgmaxResult:
+    token: np.ndarray     # N int64: argmax_j x[n, j], the lowest j among equal maxima
+    value: np.ndarray     # N float64: x[n, token[n]]
+    second: np.ndarray    # N float64: the largest x[n, j] over j != token[n] (-inf if V == 1)
+
+
+def argmax_rows(h, W, b, dtype: str = "f32", rows=None) -> ArgmaxResult:
+    """Greedy (beam 1) output layer, Algorithm 5 for every row: the best class
+    of p = W h + b, no softmax (the softmax is monotone, so the class is the
+    same as the most probable one).  The definition written out: fp64 scores
+    and numpy's argmax, which returns the first maximum (the strict '>' scan).
+    ``rows`` restricts the work to a subset of rows (results in that order).
+    """
+    h64 = widen(h, dtype)
+    if rows is not None:
+        h64 = h64[np.asarray(rows)]
+    x = logits(h64, widen(W, dtype), np.asarray(b, dtype=np.float64))
+    tok = np.argmax(x, axis=1)
+    r = np.arange(x.shape[0])
+    val = x[r, tok]
+    if x.shape[1] > 1:
+        y = x.copy()
+        y[r, tok] = -np.inf
+        second = y.max(axis=1)
+    else:
+        second = np.full(x.shape[0], -np.inf)
+    return ArgmaxResult(tok, val, second)
+
+
 def merge_softmax_stats(parts) -> tuple:
     """Combine per-shard (max, sum-of-exp relative to that max) pairs.
 

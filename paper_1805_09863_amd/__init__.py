@@ -6,5 +6,6 @@ et al., "Fast Neural Machine Translation Implementation" (WNMT 2018).  The
 work runs in the HIP kernels of ``libkbest.so`` (C ABI in include/kbest.h);
 this package only marshals arguments to it.
 """
-from .binding import (KB_BF16, KB_F32, KB_MAX_K, KBestError, abi_version, compact_batch,  # noqa: F401
-                      gather_rows, kbest_step, kbest_workspace_bytes, lib, workspace)
+from .binding import (KB_BF16, KB_F32, KB_MAX_K, KBestError, abi_version, argmax_step,  # noqa: F401
+                      argmax_workspace_bytes, compact_batch, gather_rows, kbest_step, kbest_workspace_bytes,
+                      lib, workspace)

@@ -34,6 +34,8 @@ SIGNATURES = {
     "kb_kbest_step": (_I, [_I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "kb_kbest_step_events": (_I, [_I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P,
                                   _P, _P]),
+    "kb_argmax_workspace_bytes": (_SZ, [_I, _I, _I, _I]),
+    "kb_argmax_step": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "kb_compact_batch": (_I, [_I, _I, _P, _P, _P, _P, _P, _P, _P]),
     "kb_gather_rows": (_I, [_I, _P, _P, _P, _P, _SZ, _P]),
     # decoder stand-in of the synthetic decode loop (include/kbest_standin.h)
@@ -158,6 +160,34 @@ def kbest_step(h: torch.Tensor, W: torch.Tensor, b: torch.Tensor, prev_score: to
     else:
         _check(L.kb_kbest_step_events(*args, ctypes.c_void_p(events[0]), ctypes.c_void_p(events[1])))
     return tok, par, sc
+
+
+def argmax_workspace_bytes(dtype: int, N: int, H: int, V: int) -> int:
+    return int(lib().kb_argmax_workspace_bytes(dtype, N, H, V))
+
+
+def argmax_step(h: torch.Tensor, W: torch.Tensor, b: torch.Tensor, *, out: Optional[tuple] = None,
+                ws: Optional[torch.Tensor] = None, stream=None):
+    """Greedy (beam 1) step (Algorithms 5 and 6): returns (token[N] int32, logit[N] float32),
+    the best word of every row of h @ W + b and its raw score, without a softmax."""
+    _need(h, "h", dim=2)
+    _need(W, "W", dtype=h.dtype, dim=2)
+    _need(b, "b", dtype=torch.float32, dim=1)
+    dt = _dtype_code(h)
+    N, H = h.shape
+    H2, V = W.shape
+    if H2 != H or b.shape[0] != V:
+        raise ValueError("shape mismatch among h, W, b")
+    if out is None:
+        tok = torch.empty(N, dtype=torch.int32, device=h.device)
+        val = torch.empty(N, dtype=torch.float32, device=h.device)
+    else:
+        tok, val = out
+    if ws is None:
+        ws = workspace(argmax_workspace_bytes(dt, N, H, V), h.device)
+    _check(lib().kb_argmax_step(dt, N, H, V, _ptr(h), _ptr(W), _ptr(b), _ptr(tok), _ptr(val), _ptr(ws),
+                                ws.numel() * ws.element_size(), _stream(stream)))
+    return tok, val
 
 
 def compact_batch(alive: torch.Tensor, S: int, k: int, *, out: Optional[tuple] = None, stream=None):

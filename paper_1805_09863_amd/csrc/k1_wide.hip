@@ -3,6 +3,7 @@
 
 namespace kb {
 hipError_t launch_k1_wide(int kc, dim3 grid, const K1Args& a, hipStream_t st) {
+  if (a.no_stats) return kc == 4 ? launch_k1_wide_kc<4, false>(grid, a, st) : hipErrorInvalidValue;
   switch (kc) {
     case 4: return launch_k1_wide_kc<4>(grid, a, st);
     case 8: return launch_k1_wide_kc<8>(grid, a, st);

@@ -127,7 +127,9 @@ __device__ __forceinline__ float max4(const f32x16& x, int q) {
   return fmaxf(fmax3(x[4 * q], x[4 * q + 1], x[4 * q + 2]), x[4 * q + 3]);
 }
 
-template <int KC>
+// STATS = false: the greedy (beam 1) form of Algorithm 5: only the best
+// word of every row, no softmax statistics (nothing is written to a.stats).
+template <int KC, bool STATS = true>
 __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
   using G = WideGeom;
   constexpr int BV = G::BV, BH = G::BH, BK = G::BK, WE = G::WE, HE = G::HE;
@@ -362,6 +364,10 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
         }
       const float mx = fmaxf(m0, m1);
       tmax[hb] = mx;
+      if constexpr (!STATS) {
+        done(mx);
+        continue;
+      }
       const float mnew = fmaxf(st_m[hb], mx);
       const float ml2 = mnew * kL2E;
       float s0 = st_s[hb] * exp2_fast((st_m[hb] - mnew) * kL2E), s1 = 0.f;
@@ -681,22 +687,26 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
   }
 
   // ---- this split's partial of every row: merge the four holders' statistics
+  if constexpr (STATS) {
 #pragma unroll
-  for (int hb = 0; hb < 4; ++hb) {
-    const int rl = wh * 128 + hb * 32 + col;
-    ep.u.red[rl][2 * holder + 0] = st_m[hb];
-    ep.u.red[rl][2 * holder + 1] = st_s[hb];
+    for (int hb = 0; hb < 4; ++hb) {
+      const int rl = wh * 128 + hb * 32 + col;
+      ep.u.red[rl][2 * holder + 0] = st_m[hb];
+      ep.u.red[rl][2 * holder + 1] = st_s[hb];
+    }
+    lds_barrier();
   }
-  lds_barrier();
   if (h0 + tid < a.N) {
-    float M = kStatInit;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) M = fmaxf(M, ep.u.red[tid][2 * i]);
-    float S = 0.f;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) S += ep.u.red[tid][2 * i + 1] * exp2_fast((ep.u.red[tid][2 * i] - M) * kL2E);
     const size_t row = (size_t)split * a.N + h0 + tid;
-    a.stats[row] = make_float2(M, S);
+    if constexpr (STATS) {
+      float M = kStatInit;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) M = fmaxf(M, ep.u.red[tid][2 * i]);
+      float S = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) S += ep.u.red[tid][2 * i + 1] * exp2_fast((ep.u.red[tid][2 * i] - M) * kL2E);
+      a.stats[row] = make_float2(M, S);
+    }
 #pragma unroll
     for (int j = 0; j < KC; ++j)
       if (j >= KC - k)
@@ -705,9 +715,9 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
   }
 }
 
-template <int KC>
+template <int KC, bool STATS = true>
 hipError_t launch_k1_wide_kc(dim3 grid, const K1Args& a, hipStream_t st) {
-  k1_wide<KC><<<grid, dim3(256), 0, st>>>(a);
+  k1_wide<KC, STATS><<<grid, dim3(256), 0, st>>>(a);
   return hipGetLastError();
 }
 

@@ -162,6 +162,34 @@ hipError_t launch_zero_u32(uint32_t* p, int n, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Greedy (beam 1) merge, the reduction of Algorithm 6: per row, the best
+// (score, word) over the P split lists of length 1, in the strict order
+// higher score, then lower word.  Empty list slots hold scores below every
+// real one, and the split holding the row's maximum always lists it.
+__global__ __launch_bounds__(256) void k2_argmax(const int2* __restrict__ lists, int P, int N,
+                                                 int32_t* __restrict__ tok, float* __restrict__ val) {
+  const int r = blockIdx.x * 256 + threadIdx.x;
+  if (r >= N) return;
+  float bv = -INFINITY;
+  int bi = INT_MAX;
+  for (int p = 0; p < P; ++p) {
+    const int2 e = lists[(size_t)p * N + r];
+    const float v = __int_as_float(e.x);
+    if (better(v, e.y, bv, bi)) {
+      bv = v;
+      bi = e.y;
+    }
+  }
+  tok[r] = bi;
+  val[r] = bv;
+}
+
+hipError_t launch_k2_argmax(const int2* lists, int P, int N, int32_t* tok, float* val, hipStream_t st) {
+  if (N <= 0) return hipSuccess;
+  k2_argmax<<<dim3((N + 255) / 256), dim3(256), 0, st>>>(lists, P, N, tok, val);
+  return hipGetLastError();
+}
+
 hipError_t launch_k2(const K2Args& a, hipStream_t st) {
   if (a.P > 64 * K2_LPL || a.k > 16) return hipErrorInvalidValue;
   k2_merge<<<dim3(a.S), dim3(256), 0, st>>>(a);

@@ -65,6 +65,8 @@ struct K1Args {
   int row_tiles;      // R
   int P;              // vocabulary splits
   int grp;            // row tiles per XCD group
+  int no_stats;       // 1: the statistics may be skipped (greedy argmax; only the
+                      //    256 x 256 tile kernel, k = 1, uses it)
 };
 
 // Workgroup -> (row tile, split).  Workgroups are dealt to the 8 XCDs
@@ -110,6 +112,7 @@ struct K2Args {
 };
 
 hipError_t launch_k2(const K2Args& a, hipStream_t st);
+hipError_t launch_k2_argmax(const int2* lists, int P, int N, int32_t* tok, float* val, hipStream_t st);
 
 // ---------------------------------------------------------------- K3 / gather
 hipError_t launch_compact(int S, int k, const uint8_t* alive, int32_t* keep, int32_t* kept_count,

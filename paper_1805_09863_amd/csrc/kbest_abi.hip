@@ -148,28 +148,26 @@ int validate_step(int dtype, int N, int H, int V, int k, int S) {
   return KB_OK;
 }
 
-int kbest_step_impl(int dtype, int N, int H, int V, int k, int S, const void* h, const void* W, const float* b,
-                    const float* prev, const int32_t* off, int32_t* tok, int32_t* par, float* score,
-                    float* row_lse, void* ws, size_t ws_bytes, void* stream, void* ev0, void* ev1) {
-  int st = validate_step(dtype, N, H, V, k, S);
-  if (st != KB_OK) return st;
-  if (N == 0) return ok();
-  if (!h || !W || !b || !prev || !off || !tok || !par || !score)
-    return fail(KB_ERR_INVALID_ARG, "null input or output pointer");
+// Alignment checks, plan, threshold reset and the projection kernel (K1)
+// shared by the k-best step and the greedy argmax.  On KB_OK, a1 and p
+// describe the launched projection; its partials are in the workspace.
+int launch_projection(int dtype, int N, int H, int V, int k, const void* h, const void* W, const float* b,
+                      void* ws, size_t ws_bytes, hipStream_t hs, bool no_stats, void* ev0, void* ev1,
+                      kb::K1Args& a1, Plan& p) {
   const size_t esz = dtype == KB_BF16 ? 2 : 4;
-  if (!aligned(h, esz) || !aligned(W, esz) || !aligned(b, 4) || !aligned(prev, 4))
-    return fail(KB_ERR_INVALID_ARG, "h, W, b or prev misaligned for its element type");
+  if (!aligned(h, esz) || !aligned(W, esz) || !aligned(b, 4))
+    return fail(KB_ERR_INVALID_ARG, "h, W or b misaligned for its element type");
   const int vec = dtype == KB_BF16 ? 8 : 4;
   const bool vec_ok = (H % vec == 0) && (V % vec == 0) && aligned(h, 16) && aligned(W, 16);
   const bool dma = dma_shape(dtype, H, V) && vec_ok && aligned(b, 16);
-  const Plan p = make_plan(dtype, N, H, V, k, dma);
+  p = make_plan(dtype, N, H, V, k, dma);
   const size_t need = workspace_bytes(dtype, N, H, V, k);
   if (!ws) return fail(KB_ERR_WORKSPACE, "workspace is null (%zu bytes needed)", need);
   if (!aligned(ws, 256)) return fail(KB_ERR_WORKSPACE, "workspace must be 256-byte aligned");
   if (ws_bytes < need) return fail(KB_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
   if (p.P > 256) return fail(KB_ERR_UNSUPPORTED, "too many vocabulary splits");
 
-  kb::K1Args a1{};
+  a1 = kb::K1Args{};
   a1.h = h;
   a1.W = W;
   a1.b = b;
@@ -187,14 +185,13 @@ int kbest_step_impl(int dtype, int N, int H, int V, int k, int S, const void* h,
   a1.row_tiles = p.row_tiles;
   a1.P = p.P;
   a1.grp = p.row_tiles < 4 ? p.row_tiles : 4;
-  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  a1.no_stats = (no_stats && p.layout == kb::K1_W256 && p.kc == 4) ? 1 : 0;
 
   const int n_zero = p.row_tiles * p.BH * (p.layout == kb::K1_W256 ? 1 + kGmaxSplits : 1);  // gthr (+ gmax)
   hipError_t e = kb::launch_zero_u32(a1.gthr, n_zero, hs);
   if (e != hipSuccess) return fail(KB_ERR_HIP, "threshold reset kernel launch: %s", hipGetErrorString(e));
-
   if (ev0) {
-    hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev0), hs);
+    e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev0), hs);
     if (e != hipSuccess) return fail(KB_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
   }
   e = kb::launch_k1(dtype == KB_BF16, dma, p.layout, p.kc, dim3(p.P * p.row_tiles), a1, hs);
@@ -203,6 +200,23 @@ int kbest_step_impl(int dtype, int N, int H, int V, int k, int S, const void* h,
     e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev1), hs);
     if (e != hipSuccess) return fail(KB_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
   }
+  return KB_OK;
+}
+
+int kbest_step_impl(int dtype, int N, int H, int V, int k, int S, const void* h, const void* W, const float* b,
+                    const float* prev, const int32_t* off, int32_t* tok, int32_t* par, float* score,
+                    float* row_lse, void* ws, size_t ws_bytes, void* stream, void* ev0, void* ev1) {
+  int st = validate_step(dtype, N, H, V, k, S);
+  if (st != KB_OK) return st;
+  if (N == 0) return ok();
+  if (!h || !W || !b || !prev || !off || !tok || !par || !score)
+    return fail(KB_ERR_INVALID_ARG, "null input or output pointer");
+  if (!aligned(prev, 4)) return fail(KB_ERR_INVALID_ARG, "prev misaligned");
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  kb::K1Args a1;
+  Plan p;
+  st = launch_projection(dtype, N, H, V, k, h, W, b, ws, ws_bytes, hs, false, ev0, ev1, a1, p);
+  if (st != KB_OK) return st;
 
   kb::K2Args a2{};
   a2.stats = a1.stats;
@@ -218,7 +232,7 @@ int kbest_step_impl(int dtype, int N, int H, int V, int k, int S, const void* h,
   a2.par = par;
   a2.score = score;
   a2.row_lse = row_lse;
-  e = kb::launch_k2(a2, hs);
+  hipError_t e = kb::launch_k2(a2, hs);
   if (e != hipSuccess) return fail(KB_ERR_HIP, "merge kernel launch: %s", hipGetErrorString(e));
   return ok();
 }
@@ -261,6 +275,27 @@ int kb_kbest_step_events(int dtype, int N, int H, int V, int k, int S, const voi
   return kbest_step_impl(dtype, N, H, V, k, S, h, W, b, prev_score, sent_offsets, out_token, out_parent,
                          out_score, out_row_lse, workspace, workspace_bytes, stream, proj_begin_event,
                          proj_end_event);
+}
+
+size_t kb_argmax_workspace_bytes(int dtype, int N, int H, int V) {
+  if (validate_step(dtype, N, H, V, 1, N > 0 ? 1 : 0) != KB_OK || N == 0) return 0;
+  return workspace_bytes(dtype, N, H, V, 1);
+}
+
+int kb_argmax_step(int dtype, int N, int H, int V, const void* h, const void* W, const float* b, int32_t* out_token,
+                   float* out_logit, void* workspace, size_t workspace_bytes, void* stream) {
+  int st = validate_step(dtype, N, H, V, 1, N > 0 ? 1 : 0);
+  if (st != KB_OK) return st;
+  if (N == 0) return ok();
+  if (!h || !W || !b || !out_token || !out_logit) return fail(KB_ERR_INVALID_ARG, "null input or output pointer");
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  kb::K1Args a1;
+  Plan p;
+  st = launch_projection(dtype, N, H, V, 1, h, W, b, workspace, workspace_bytes, hs, true, nullptr, nullptr, a1, p);
+  if (st != KB_OK) return st;
+  hipError_t e = kb::launch_k2_argmax(a1.lists, p.P, N, out_token, out_logit, hs);
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "argmax merge kernel launch: %s", hipGetErrorString(e));
+  return ok();
 }
 
 int kb_compact_batch(int S, int k, const uint8_t* alive, int32_t* keep_idx, int32_t* kept_count,

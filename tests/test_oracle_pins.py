@@ -256,6 +256,43 @@ def test_argmax_only_and_sharded():
             assert ko.argmax_sharded(p, b, shards) == want
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_argmax_rows_is_alg5_per_row(dtype):
+    # The vectorised greedy oracle against the Algorithm 5 loop (strict '>')
+    # and the Algorithm 6 sharded reduction, row by row, on the exact widened
+    # scores; duplicated columns force exact ties, which the lower word wins.
+    inp = wl.make_step(H=24, V=300, k=1, S=20, beam=1, dtype=dtype, seed=31)
+    W = inp.W.copy()
+    W[:, 150:180] = W[:, 10:40]                 # twins of 30 columns (b differs: copy it too)
+    b = inp.b.copy()
+    b[150:180] = b[10:40]
+    res = ko.argmax_rows(inp.h, W, b, dtype)
+    x = ko.widen(inp.h, dtype) @ ko.widen(W, dtype) + b.astype(np.float64)[None, :]
+    for n in range(inp.N):
+        want = ko.argmax_only(x[n], np.zeros(inp.V))
+        assert res.token[n] == want
+        assert ko.argmax_sharded(x[n], np.zeros(inp.V), 7) == want
+        assert res.value[n] == x[n, want]
+        assert res.second[n] == np.max(np.delete(x[n], want))
+        assert want < 150 or want >= 180          # a twin never beats its original
+
+
+def test_argmax_rows_brute_force_and_subset():
+    # Tiny inputs in plain Python floats (math.fsum dot products); a subset of
+    # rows gives the same answers as the full call.
+    g = np.random.default_rng(12)
+    h = np.round(g.normal(0, 1, (7, 3)) * 4) / 4
+    W = np.round(g.normal(0, 1, (3, 11)) * 4) / 4
+    b = np.round(g.normal(0, 1, 11) * 4) / 4
+    res = ko.argmax_rows(h.astype(np.float32), W.astype(np.float32), b.astype(np.float32))
+    for n in range(7):
+        sc = [math.fsum([float(h[n, i]) * float(W[i, j]) for i in range(3)] + [float(b[j])]) for j in range(11)]
+        best = max(range(11), key=lambda j: (sc[j], -j))
+        assert res.token[n] == best and res.value[n] == sc[best]
+    sub = ko.argmax_rows(h.astype(np.float32), W.astype(np.float32), b.astype(np.float32), rows=[5, 1])
+    assert list(sub.token) == [res.token[5], res.token[1]]
+
+
 def test_merge_softmax_stats_any_sharding():
     g = np.random.default_rng(8)
     x = g.normal(0, 3, 3000)
