@@ -157,6 +157,37 @@ int kb_argmax_step(int dtype, int N, int H, int V, const void* h, const void* W,
                    void* stream);
 
 /*
+ * kb_kbest_step_unfused -- the same step as kb_kbest_step computed by the
+ * unfused baseline the paper compares against (Section 3, the breakdown into
+ * multiplication, add bias, softmax and k-best extraction): every stage is a
+ * kernel of its own and the N x V scores are stored in the workspace between
+ * stages.
+ *   mode 0   Algorithm 3: p = W h; AddBias; Softmax in three passes (max,
+ *            sum, normalise, in place); Find-Best extended to the k best of
+ *            every row (on probabilities); beam merge.
+ *   mode 1   Algorithm 4 over the stored scores: p = W h; one fused pass per
+ *            row (bias, running max and sum, k best); beam merge.
+ * Arguments and results are those of kb_kbest_step (same tie rules; scores
+ * agree within float32 rounding).  Supported shapes: bf16, H % 128 == 0,
+ * V % 8 == 0, V >= 256, h, W, b 16-byte aligned (else KB_ERR_UNSUPPORTED /
+ * KB_ERR_INVALID_ARG).  The workspace (kb_unfused_workspace_bytes; about
+ * N * V * 4 bytes) holds the scores.
+ *   stage_events  nullable array of n_events hipEvent_t, recorded on the
+ *                 stream at the stage boundaries: mode 0: before the
+ *                 projection, after it, after AddBias, after Softmax, after
+ *                 the k-best, after the merge (6); mode 1: before, after the
+ *                 projection, after the fused pass, after the merge (4).
+ *                 Events beyond n_events or NULL entries are skipped.
+ */
+size_t kb_unfused_workspace_bytes(int dtype, int N, int H, int V, int k, int S);
+int kb_kbest_step_unfused(int mode, int dtype, int N, int H, int V, int k, int S, const void* h,
+                          const void* W, const float* b, const float* prev_score,
+                          const int32_t* sent_offsets, int32_t* out_token, int32_t* out_parent,
+                          float* out_score, float* out_row_lse, void* workspace,
+                          size_t workspace_bytes, void* const* stage_events, int n_events,
+                          void* stream);
+
+/*
  * kb_compact_batch -- remove finished hypotheses from the batch (Section 2.1,
  * Algorithm 2: after each Decode, every hypothesis that produced EOS leaves
  * the batch; decoding stops when the batch is empty).

@@ -36,6 +36,9 @@ SIGNATURES = {
                                   _P, _P]),
     "kb_argmax_workspace_bytes": (_SZ, [_I, _I, _I, _I]),
     "kb_argmax_step": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "kb_unfused_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I, _I]),
+    "kb_kbest_step_unfused": (_I, [_I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ,
+                                   _P, _I, _P]),
     "kb_compact_batch": (_I, [_I, _I, _P, _P, _P, _P, _P, _P, _P]),
     "kb_gather_rows": (_I, [_I, _P, _P, _P, _P, _SZ, _P]),
     # decoder stand-in of the synthetic decode loop (include/kbest_standin.h)
@@ -188,6 +191,42 @@ def argmax_step(h: torch.Tensor, W: torch.Tensor, b: torch.Tensor, *, out: Optio
     _check(lib().kb_argmax_step(dt, N, H, V, _ptr(h), _ptr(W), _ptr(b), _ptr(tok), _ptr(val), _ptr(ws),
                                 ws.numel() * ws.element_size(), _stream(stream)))
     return tok, val
+
+
+def unfused_workspace_bytes(dtype: int, N: int, H: int, V: int, k: int, S: int) -> int:
+    return int(lib().kb_unfused_workspace_bytes(dtype, N, H, V, k, S))
+
+
+def kbest_step_unfused(h: torch.Tensor, W: torch.Tensor, b: torch.Tensor, prev_score: torch.Tensor,
+                       sent_offsets: torch.Tensor, k: int, *, mode: int = 0, out: Optional[tuple] = None,
+                       ws: Optional[torch.Tensor] = None, row_lse: Optional[torch.Tensor] = None,
+                       events: Optional[list] = None, stream=None):
+    """The unfused baseline of kbest_step (mode 0: Algorithm 3; mode 1: Algorithm 4
+    over stored scores); ``events`` is a list of raw hipEvent_t handles recorded
+    at the stage boundaries (see include/kbest.h)."""
+    _need(h, "h", dim=2)
+    _need(W, "W", dtype=h.dtype, dim=2)
+    _need(b, "b", dtype=torch.float32, dim=1)
+    _need(prev_score, "prev_score", dtype=torch.float32, dim=1)
+    _need(sent_offsets, "sent_offsets", dtype=torch.int32, dim=1)
+    dt = _dtype_code(h)
+    N, H = h.shape
+    V = W.shape[1]
+    S = sent_offsets.shape[0] - 1
+    if out is None:
+        out = tuple(torch.empty((S, k), dtype=t, device=h.device)
+                    for t in (torch.int32, torch.int32, torch.float32))
+    tok, par, sc = out
+    if ws is None:
+        ws = workspace(unfused_workspace_bytes(dt, N, H, V, k, S), h.device)
+    ev = None
+    if events:
+        ev = (ctypes.c_void_p * len(events))(*[ctypes.c_void_p(e) for e in events])
+    _check(lib().kb_kbest_step_unfused(mode, dt, N, H, V, k, S, _ptr(h), _ptr(W), _ptr(b), _ptr(prev_score),
+                                       _ptr(sent_offsets), _ptr(tok), _ptr(par), _ptr(sc), _ptr(row_lse),
+                                       _ptr(ws), ws.numel() * ws.element_size(), ev,
+                                       len(events) if events else 0, _stream(stream)))
+    return tok, par, sc
 
 
 def compact_batch(alive: torch.Tensor, S: int, k: int, *, out: Optional[tuple] = None, stream=None):

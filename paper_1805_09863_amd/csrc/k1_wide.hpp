@@ -127,10 +127,18 @@ __device__ __forceinline__ float max4(const f32x16& x, int q) {
   return fmaxf(fmax3(x[4 * q], x[4 * q + 1], x[4 * q + 2]), x[4 * q + 3]);
 }
 
-// STATS = false: the greedy (beam 1) form of Algorithm 5: only the best
-// word of every row, no softmax statistics (nothing is written to a.stats).
-template <int KC, bool STATS = true>
+// What the kernel does with its tiles of scores.
+enum WideMode {
+  kWideKBest = 0,   // bias, softmax statistics, per-split k-best (the fused step)
+  kWideArgmax = 1,  // the greedy (beam 1) form of Algorithm 5: only the best word of
+                    // every row, no softmax statistics (nothing written to a.stats)
+  kWideStore = 2,   // the plain projection p = W h: every score stored to a.logits
+                    // (N x V float32, row-major), nothing else (the unfused baseline)
+};
+
+template <int KC, int MODE = kWideKBest>
 __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
+  constexpr bool STATS = MODE == kWideKBest;
   using G = WideGeom;
   constexpr int BV = G::BV, BH = G::BH, BK = G::BK, WE = G::WE, HE = G::HE;
   __shared__ __attribute__((aligned(16))) uint16_t S0[WE + HE], S1[WE + HE], S2[WE + HE], S3[WE + HE];
@@ -289,7 +297,8 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int wl = wv * 128 + vb * 32 + 8 * i + 4 * half;
-        const float4 bb = *reinterpret_cast<const float4*>(&ep.bias[par][wl]);
+        float4 bb = *reinterpret_cast<const float4*>(&ep.bias[par][wl]);
+        if constexpr (MODE == kWideStore) bb = make_float4(0.f, 0.f, 0.f, 0.f);  // p = W h only
         bv[4 * i + 0] = bb.x;
         bv[4 * i + 1] = bb.y;
         bv[4 * i + 2] = bb.z;
@@ -577,6 +586,27 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
     }
   };
 
+  // ---- the plain projection: the tile's scores to a.logits (rows < N,
+  // words < V; each lane holds 4 consecutive words of a row per 16-byte store)
+  auto store_tile = [&](int ti) {
+    const int v0 = (split + ti * a.P) * BV;
+#pragma unroll
+    for (int hb = 0; hb < 4; ++hb) {
+      const int n = h0 + wh * 128 + hb * 32 + col;
+#pragma unroll
+      for (int vb = 0; vb < 4; ++vb) {
+        opaque(acc[vb][hb]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int w = v0 + wv * 128 + vb * 32 + 8 * i + 4 * half;
+          if (n < a.N && w < a.V)
+            *reinterpret_cast<float4*>(a.logits + (size_t)n * a.V + w) =
+                make_float4(acc[vb][hb][4 * i], acc[vb][hb][4 * i + 1], acc[vb][hb][4 * i + 2], acc[vb][hb][4 * i + 3]);
+        }
+      }
+    }
+  };
+
   // ---- the stage pipeline
   uint16_t* const bufs[4] = {S0, S1, S2, S3};
   Frag F0, F1;
@@ -678,7 +708,10 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
     body(I1{}, RD{});
     body(I2{}, RD{});
     body(I3{}, NR{});
-    epilogue(ti);
+    if constexpr (MODE == kWideStore)
+      store_tile(ti);
+    else
+      epilogue(ti);
     if (ti + 1 < nt) {
       init_acc(ti + 1);
 #pragma unroll
@@ -686,6 +719,7 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
     }
   }
 
+  if constexpr (MODE == kWideStore) return;
   // ---- this split's partial of every row: merge the four holders' statistics
   if constexpr (STATS) {
 #pragma unroll
@@ -715,9 +749,9 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
   }
 }
 
-template <int KC, bool STATS = true>
+template <int KC, int MODE = kWideKBest>
 hipError_t launch_k1_wide_kc(dim3 grid, const K1Args& a, hipStream_t st) {
-  k1_wide<KC, STATS><<<grid, dim3(256), 0, st>>>(a);
+  k1_wide<KC, MODE><<<grid, dim3(256), 0, st>>>(a);
   return hipGetLastError();
 }
 

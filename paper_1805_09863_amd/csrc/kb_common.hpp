@@ -67,6 +67,7 @@ struct K1Args {
   int grp;            // row tiles per XCD group
   int no_stats;       // 1: the statistics may be skipped (greedy argmax; only the
                       //    256 x 256 tile kernel, k = 1, uses it)
+  float* logits;      // N x V scores p = W h (the unfused baseline's projection only)
 };
 
 // Workgroup -> (row tile, split).  Workgroups are dealt to the 8 XCDs
@@ -120,6 +121,14 @@ hipError_t launch_compact(int S, int k, const uint8_t* alive, int32_t* keep, int
 
 hipError_t launch_gather(int n_max, const int32_t* n_dev, const int32_t* idx, const void* src,
                          void* dst, size_t row_bytes, hipStream_t st);
+
+// ---------------------------------------------------------------- unfused baseline
+hipError_t launch_k1_wide_store(dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_uf_add_bias(float* x, const float* b, int N, int V, hipStream_t st);
+hipError_t launch_uf_softmax3(float* x, int N, int V, float* row_lse, hipStream_t st);
+hipError_t launch_uf_kbest_rows(const float* p, int N, int V, int k, float2* stats, int2* lists, hipStream_t st);
+hipError_t launch_uf_fused_rows(const float* x, const float* b, int N, int V, int k, float2* stats, int2* lists,
+                                hipStream_t st);
 
 // ---------------------------------------------------------------- decoder stand-in
 hipError_t launch_standin_alive(int S, int k, int t, const int32_t* sid, const int32_t* lengths, uint8_t* alive,

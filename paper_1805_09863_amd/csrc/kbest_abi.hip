@@ -239,6 +239,50 @@ int kbest_step_impl(int dtype, int N, int H, int V, int k, int S, const void* h,
 
 }  // namespace
 
+// ---- the unfused baseline (Algorithm 3; Algorithm 4 over stored scores)
+namespace {
+struct UfPlan {
+  kb::K1Args a1;
+  int row_tiles, P;
+  size_t logits_off, stats_off, lists_off, gthr_off, bytes;
+};
+
+bool uf_shape(int dtype, int H, int V) { return dma_shape(dtype, H, V) && V >= kWideMinCols; }
+
+UfPlan uf_plan(int N, int H, int V, int k) {
+  UfPlan u{};
+  u.row_tiles = (N + 255) / 256;
+  const int n_vtiles = (V + 255) / 256;
+  int P = kTargetCUs / u.row_tiles;
+  if (P < 1) P = 1;
+  if (P > n_vtiles) P = n_vtiles;
+  const int tps = (n_vtiles + P - 1) / P;
+  u.P = (n_vtiles + tps - 1) / tps;
+  u.logits_off = 0;
+  u.stats_off = align_up((size_t)N * V * sizeof(float), 256);
+  u.lists_off = align_up(u.stats_off + (size_t)N * sizeof(float2), 256);
+  u.gthr_off = align_up(u.lists_off + (size_t)N * k * sizeof(int2), 256);
+  u.bytes = align_up(u.gthr_off + (size_t)u.row_tiles * 256 * sizeof(uint32_t), 256);
+  u.a1.N = N;
+  u.a1.H = H;
+  u.a1.V = V;
+  u.a1.k = k;
+  u.a1.tps = tps;
+  u.a1.n_vtiles = n_vtiles;
+  u.a1.vec_ok = 1;
+  u.a1.row_tiles = u.row_tiles;
+  u.a1.P = u.P;
+  u.a1.grp = u.row_tiles < 4 ? u.row_tiles : 4;
+  return u;
+}
+
+int record(void* const* ev, int n_ev, int i, hipStream_t hs) {
+  if (!ev || i >= n_ev || !ev[i]) return KB_OK;
+  hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev[i]), hs);
+  return e == hipSuccess ? KB_OK : fail(KB_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+}
+}  // namespace
+
 extern "C" {
 
 int kb_abi_version(void) { return KB_ABI_VERSION; }
@@ -275,6 +319,82 @@ int kb_kbest_step_events(int dtype, int N, int H, int V, int k, int S, const voi
   return kbest_step_impl(dtype, N, H, V, k, S, h, W, b, prev_score, sent_offsets, out_token, out_parent,
                          out_score, out_row_lse, workspace, workspace_bytes, stream, proj_begin_event,
                          proj_end_event);
+}
+
+
+size_t kb_unfused_workspace_bytes(int dtype, int N, int H, int V, int k, int S) {
+  if (validate_step(dtype, N, H, V, k, S) != KB_OK || N == 0 || !uf_shape(dtype, H, V)) return 0;
+  return uf_plan(N, H, V, k).bytes;
+}
+
+int kb_kbest_step_unfused(int mode, int dtype, int N, int H, int V, int k, int S, const void* h, const void* W,
+                          const float* b, const float* prev_score, const int32_t* sent_offsets, int32_t* out_token,
+                          int32_t* out_parent, float* out_score, float* out_row_lse, void* workspace,
+                          size_t workspace_bytes, void* const* stage_events, int n_events, void* stream) {
+  if (mode != 0 && mode != 1) return fail(KB_ERR_INVALID_ARG, "mode %d: 0 (Algorithm 3) or 1 (Algorithm 4)", mode);
+  int st = validate_step(dtype, N, H, V, k, S);
+  if (st != KB_OK) return st;
+  if (N == 0) return ok();
+  if (!uf_shape(dtype, H, V))
+    return fail(KB_ERR_UNSUPPORTED, "the unfused baseline needs bf16, H %% 128 == 0, V %% 8 == 0 and V >= 256");
+  if (!h || !W || !b || !prev_score || !sent_offsets || !out_token || !out_parent || !out_score)
+    return fail(KB_ERR_INVALID_ARG, "null input or output pointer");
+  if (!aligned(h, 16) || !aligned(W, 16) || !aligned(b, 16) || !aligned(prev_score, 4))
+    return fail(KB_ERR_INVALID_ARG, "h, W and b must be 16-byte aligned, prev 4-byte aligned");
+  UfPlan u = uf_plan(N, H, V, k);
+  if (!workspace) return fail(KB_ERR_WORKSPACE, "workspace is null (%zu bytes needed)", u.bytes);
+  if (!aligned(workspace, 256)) return fail(KB_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (workspace_bytes < u.bytes) return fail(KB_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, u.bytes);
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  float* x = reinterpret_cast<float*>(ws + u.logits_off);
+  float2* stats = reinterpret_cast<float2*>(ws + u.stats_off);
+  int2* lists = reinterpret_cast<int2*>(ws + u.lists_off);
+  u.a1.h = h;
+  u.a1.W = W;
+  u.a1.b = b;
+  u.a1.logits = x;
+  u.a1.gthr = reinterpret_cast<uint32_t*>(ws + u.gthr_off);  // read by the kernel's pipeline, not used
+  u.a1.gmax = u.a1.gthr;
+  u.a1.stats = stats;
+  u.a1.lists = lists;
+  hipError_t e;
+#define UF_CHECK(call, what)                                                   \
+  do {                                                                         \
+    e = (call);                                                                \
+    if (e != hipSuccess) return fail(KB_ERR_HIP, what ": %s", hipGetErrorString(e)); \
+  } while (0)
+  if ((st = record(stage_events, n_events, 0, hs)) != KB_OK) return st;
+  UF_CHECK(kb::launch_k1_wide_store(dim3(u.P * u.row_tiles), u.a1, hs), "projection kernel launch");
+  if ((st = record(stage_events, n_events, 1, hs)) != KB_OK) return st;
+  if (mode == 0) {
+    UF_CHECK(kb::launch_uf_add_bias(x, b, N, V, hs), "bias kernel launch");
+    if ((st = record(stage_events, n_events, 2, hs)) != KB_OK) return st;
+    UF_CHECK(kb::launch_uf_softmax3(x, N, V, out_row_lse, hs), "softmax kernel launch");
+    if ((st = record(stage_events, n_events, 3, hs)) != KB_OK) return st;
+    UF_CHECK(kb::launch_uf_kbest_rows(x, N, V, k, stats, lists, hs), "k-best kernel launch");
+  } else {
+    UF_CHECK(kb::launch_uf_fused_rows(x, b, N, V, k, stats, lists, hs), "fused pass launch");
+  }
+  if ((st = record(stage_events, n_events, mode == 0 ? 4 : 2, hs)) != KB_OK) return st;
+  kb::K2Args a2{};
+  a2.stats = stats;
+  a2.lists = lists;
+  a2.P = 1;
+  a2.N = N;
+  a2.V = V;
+  a2.k = k;
+  a2.S = S;
+  a2.prev = prev_score;
+  a2.off = sent_offsets;
+  a2.tok = out_token;
+  a2.par = out_parent;
+  a2.score = out_score;
+  a2.row_lse = mode == 0 ? nullptr : out_row_lse;  // Algorithm 3's softmax wrote it
+  UF_CHECK(kb::launch_k2(a2, hs), "merge kernel launch");
+#undef UF_CHECK
+  if ((st = record(stage_events, n_events, mode == 0 ? 5 : 3, hs)) != KB_OK) return st;
+  return ok();
 }
 
 size_t kb_argmax_workspace_bytes(int dtype, int N, int H, int V) {

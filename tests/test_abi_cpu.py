@@ -119,3 +119,24 @@ def test_gather_validation():
     assert L.kb_gather_rows(4, None, None, FAKE, FAKE, 16, None) == KB_ERR_INVALID_ARG
     assert L.kb_gather_rows(4, None, FAKE, ctypes.c_void_p(0x1002), FAKE, 16, None) == KB_ERR_INVALID_ARG
     assert L.kb_gather_rows(0, None, None, None, None, 16, None) == KB_OK
+
+
+def test_argmax_and_unfused_argument_checks():
+    L = binding.lib()
+    # greedy step
+    assert L.kb_argmax_workspace_bytes(1, 0, 16, 100) == 0
+    assert L.kb_argmax_workspace_bytes(1, 10, 128, 1000) > 0
+    assert L.kb_argmax_step(7, 10, 128, 1000, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == KB_ERR_INVALID_ARG
+    assert L.kb_argmax_step(1, 0, 128, 1000, None, None, None, None, None, None, 0, None) == KB_OK
+    assert L.kb_argmax_step(1, 10, 128, 1000, FAKE, FAKE, FAKE, None, FAKE, FAKE, 1 << 30, None) == KB_ERR_INVALID_ARG
+    assert L.kb_argmax_step(1, 10, 128, 1000, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 16, None) == KB_ERR_WORKSPACE
+    # unfused baseline
+    assert L.kb_unfused_workspace_bytes(1, 3072, 1024, 90000, 12, 256) >= 3072 * 90000 * 4
+    assert L.kb_unfused_workspace_bytes(0, 64, 128, 1000, 5, 8) == 0          # float32: not supported
+    args = [FAKE] * 10 + [1 << 40, None, 0, None]
+    assert L.kb_kbest_step_unfused(2, 1, 10, 128, 1000, 5, 2, *args) == KB_ERR_INVALID_ARG   # mode
+    assert L.kb_kbest_step_unfused(0, 1, 10, 100, 1000, 5, 2, *args) == KB_ERR_UNSUPPORTED   # H % 128
+    assert L.kb_kbest_step_unfused(0, 1, 10, 128, 200, 5, 2, *args) == KB_ERR_UNSUPPORTED    # V < 256
+    small = [FAKE] * 10 + [64, None, 0, None]
+    assert L.kb_kbest_step_unfused(1, 1, 10, 128, 1000, 5, 2, *small) == KB_ERR_WORKSPACE
+    assert L.kb_kbest_step_unfused(0, 1, 0, 128, 1000, 5, 0, *args) == KB_OK                 # empty batch
