@@ -159,6 +159,171 @@ def decode_loop_bench(torch, np, reps: int = 2):
     return out
 
 
+def _mean_stage_ms(ev, sets):
+    """Mean over repetitions of the gaps between consecutive events of each set."""
+    n = len(sets[0]) - 1
+    return [sum(ev.elapsed_ms(es[i], es[i + 1]) for es in sets) / len(sets) for i in range(n)]
+
+
+def ablation_bench(torch, np, kb, reps: int = 10):
+    """Time per stage of one step, fused against the unfused baselines (the
+    paper's breakdown into multiplication, add bias, softmax and k-best),
+    256 sentences at V=90k (H=1024, bf16, Zipf bias) with beam = k = 1, 3, 9."""
+    from synth import workloads as wl
+    ev = HipEvents()
+    S, H, V = 256, 1024, 90000
+    big = wl.make_step(H=H, V=V, k=9, S=S, beam=9, dtype="bf16", seed=wl.SEED_BASE + 77, bias="zipf")
+    W = torch.from_numpy(big.W.view(np.int16)).view(torch.bfloat16).cuda()
+    b = torch.from_numpy(big.b).cuda()
+    rows = []
+    for beam in (1, 3, 9):
+        N, k = S * beam, beam
+        h = torch.from_numpy(np.ascontiguousarray(big.h[:N]).view(np.int16)).view(torch.bfloat16).cuda()
+        prev = torch.from_numpy(np.ascontiguousarray(big.prev[:N])).cuda()
+        off = torch.from_numpy(wl.uniform_offsets(S, beam)).cuda()
+        out = tuple(torch.empty((S, k), dtype=t, device="cuda") for t in (torch.int32, torch.int32, torch.float32))
+        ws_f = kb.workspace(kb.kbest_workspace_bytes(kb.KB_BF16, N, H, V, k, S))
+        ws_u = kb.workspace(kb.unfused_workspace_bytes(kb.KB_BF16, N, H, V, k, S))
+        res = {"beam": beam, "k": k, "N": N}
+        # fused: reset kernel, [event] K1 [event] K2 [event]  (the 12 KB threshold reset before
+        # the first event, a few microseconds, is left out: the event before it would also
+        # time the host's launch work on an idle GPU)
+        sets = [[ev.create() for _ in range(3)] for _ in range(reps)]
+        for i in range(2 + reps):
+            es = sets[i - 2] if i >= 2 else sets[0]
+            kb.kbest_step(h, W, b, prev, off, k, out=out, ws=ws_f, events=(es[0], es[1]))
+            ev.rt.hipEventRecord(ctypes.c_void_p(es[2]), ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+            torch.cuda.synchronize()
+        g = _mean_stage_ms(ev, sets)
+        res["fused_ms"] = {"projection_bias_softmax_kbest": g[0], "merge": g[1], "total": sum(g)}
+        for mode, names in ((0, ["multiplication", "add_bias", "softmax", "kbest", "merge"]),
+                            (1, ["multiplication", "fused_pass", "merge"])):
+            sets = [[ev.create() for _ in range(len(names) + 1)] for _ in range(reps)]
+            for i in range(2 + reps):
+                es = sets[i - 2] if i >= 2 else sets[0]
+                kb.kbest_step_unfused(h, W, b, prev, off, k, mode=mode, out=out, ws=ws_u, events=es)
+                torch.cuda.synchronize()
+            g = _mean_stage_ms(ev, sets)
+            d = dict(zip(names, g))
+            d["total"] = sum(g)
+            res["alg3_unfused_ms" if mode == 0 else "alg4_over_stored_ms"] = d
+        rows.append(res)
+        log(f"ablation beam {beam}: fused {res['fused_ms']['total']:.3f} ms, "
+            f"Alg.4 over stored {res['alg4_over_stored_ms']['total']:.3f} ms, "
+            f"Alg.3 {res['alg3_unfused_ms']['total']:.3f} ms")
+        del ws_u
+    # greedy decoding (Algorithm 5, no softmax) against the k = 1 step, beam 1,
+    # back-to-back launches (mean per call)
+    greedy = []
+    for N in (256, 1280, 2304):
+        h = torch.from_numpy(np.ascontiguousarray(big.h[:N]).view(np.int16)).view(torch.bfloat16).cuda()
+        prev = torch.from_numpy(np.ascontiguousarray(big.prev[:N])).cuda()
+        off = torch.from_numpy(wl.uniform_offsets(N, 1)).cuda()
+        out = tuple(torch.empty((N, 1), dtype=t, device="cuda") for t in (torch.int32, torch.int32, torch.float32))
+        tv = (torch.empty(N, dtype=torch.int32, device="cuda"), torch.empty(N, dtype=torch.float32, device="cuda"))
+        ws_f = kb.workspace(kb.kbest_workspace_bytes(kb.KB_BF16, N, H, V, 1, N))
+        ws_a = kb.workspace(kb.argmax_workspace_bytes(kb.KB_BF16, N, H, V))
+        g = {"N": N}
+        for name, fn in (("kbest_k1", lambda: kb.kbest_step(h, W, b, prev, off, 1, out=out, ws=ws_f)),
+                         ("greedy_argmax", lambda: kb.argmax_step(h, W, b, out=tv, ws=ws_a))):
+            for _ in range(3):
+                fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(reps * 2):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            g[name + "_ms"] = e0.elapsed_time(e1) / (reps * 2)
+        log(f"greedy N={N}: k=1 step {g['kbest_k1_ms']:.3f} ms, argmax {g['greedy_argmax_ms']:.3f} ms")
+        greedy.append(g)
+    return {"workload": f"S={S} sentences x beam 1/3/9 (k = beam), H={H}, V={V}, bf16, Zipf bias",
+            "reps": reps, "rows": rows, "greedy_beam1": greedy}
+
+
+def sweep_bench(torch, np, kb):
+    """Step time against the number of rows, the per-step time of a 1280-sentence
+    decode (compacted and naive), and decode throughput against the number of
+    sentences (beam 5, H=1024, V=50k, bf16)."""
+    from paper_1805_09863_amd.decode import decode_loop
+    from synth import workloads as wl
+    S0, T, beam, H = 1280, 60, 5, 1024
+    work = wl.make_loop_workload(S=S0)
+    V = work.V
+    W = torch.from_numpy(work.W.view(np.int16)).view(torch.bfloat16).cuda()
+    b = torch.from_numpy(work.b).cuda()
+    gen = torch.Generator(device="cuda").manual_seed(wl.SEED_BASE + 5)
+    h_table = torch.empty((S0 * T * beam, H), dtype=torch.bfloat16, device="cuda")
+    for i in range(0, h_table.shape[0], 65536):   # the decoder stand-in's states, drawn on the device
+        h_table[i:i + 65536] = torch.randn((min(65536, h_table.shape[0] - i), H), generator=gen, device="cuda")
+    L = torch.from_numpy(work.lengths).cuda()
+    p0 = torch.from_numpy(work.prev0).cuda()
+    out = {"workload": f"beam {beam}, H={H}, V={V}, bf16, uniform bias, lengths ~U{{5..60}}"}
+    # (1) one step against the number of rows
+    step = []
+    for N in (5, 10, 25, 50, 100, 200, 320, 500, 640, 1000, 1280, 2000, 2560, 3200, 4096):
+        Sx = (N + beam - 1) // beam
+        h = h_table[:N].contiguous()
+        prev = torch.zeros(N, device="cuda")
+        off = torch.tensor([min(i * beam, N) for i in range(Sx + 1)], dtype=torch.int32, device="cuda")
+        ws = kb.workspace(kb.kbest_workspace_bytes(kb.KB_BF16, N, H, V, beam, Sx))
+        for _ in range(3):
+            kb.kbest_step(h, W, b, prev, off, beam, ws=ws)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(20):
+            kb.kbest_step(h, W, b, prev, off, beam, ws=ws)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / 20
+        step.append({"N": N, "ms": ms, "hyps_per_s": N / (ms * 1e-3)})
+        log(f"sweep step N={N}: {ms * 1e3:.1f} us")
+    out["step_vs_rows"] = step
+    # (2) per-step time of the 1280-sentence decode
+    curves = {}
+    for compact in (True, False):
+        marks = []
+
+        def on_step(t, st, marks=marks):
+            e = torch.cuda.Event(enable_timing=True)
+            e.record()
+            marks.append((st["N"], e))
+        decode_loop(h_table, W, b, L, p0, beam, T, compact=compact)          # warm-up
+        torch.cuda.synchronize()
+        start = torch.cuda.Event(enable_timing=True)
+        start.record()
+        decode_loop(h_table, W, b, L, p0, beam, T, compact=compact, on_step=on_step)
+        torch.cuda.synchronize()
+        prev_e, per = start, []
+        for n, e in marks:
+            per.append({"rows": n, "ms": prev_e.elapsed_time(e)})
+            prev_e = e
+        curves["compacted" if compact else "naive"] = per
+    out["per_step_1280"] = curves
+    # (3) decode throughput against the number of sentences
+    by_s = []
+    for Sx in (1, 2, 5, 10, 20, 50, 100, 200, 500, 1000, 1280):
+        r = {"S": Sx}
+        for compact in (True, False):
+            tab = h_table[:Sx * T * beam]
+            decode_loop(tab, W, b, L[:Sx], p0[:Sx * beam], beam, T, compact=compact)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            st = decode_loop(tab, W, b, L[:Sx], p0[:Sx * beam], beam, T, compact=compact)
+            torch.cuda.synchronize()
+            dt = time.perf_counter() - t0
+            r["compacted" if compact else "naive"] = {"seconds": dt, "live_rows": st.total_rows,
+                                                      "live_hyps_per_s": st.total_rows / dt,
+                                                      "sentences_per_s": Sx / dt}
+        log(f"sweep S={Sx}: compacted {r['compacted']['seconds'] * 1e3:.2f} ms, "
+            f"naive {r['naive']['seconds'] * 1e3:.2f} ms")
+        by_s.append(r)
+    out["decode_vs_sentences"] = by_s
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -168,6 +333,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode-loop", action="store_true")
     ap.add_argument("--print-k1-hash", action="store_true", help="print the projection-kernel source hash and exit")
+    ap.add_argument("--ablation", action="store_true",
+                    help="only time the fused step against the unfused baselines, stage by stage "
+                         "(beams 1/3/9 at V=90k), print that as the JSON line and exit")
+    ap.add_argument("--sweep", action="store_true",
+                    help="only run the row-count and batch-size sweeps and the per-step curves of a "
+                         "1280-sentence decode, print them as the JSON line and exit")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB three times (to scale HBM "
                          "byte counters against a kernel of known traffic), then exit")
@@ -197,6 +368,14 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "launches": 3}))
+        return
+    if args.ablation or args.sweep:
+        kb.lib()
+        res = {"metric": "fused vs unfused step time by stage" if args.ablation else "sweeps",
+               "unit": "ms", "data": "synthetic (seeded)", "n_gpus": 1}
+        res["ablation" if args.ablation else "sweep"] = (ablation_bench if args.ablation else sweep_bench)(
+            torch, np, kb)
+        print(json.dumps(res), flush=True)
         return
     kb.lib()
     log("generating the V=90k workload ...")

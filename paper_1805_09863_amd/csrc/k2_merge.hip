@@ -164,15 +164,18 @@ hipError_t launch_zero_u32(uint32_t* p, int n, hipStream_t st) {
 
 // Greedy (beam 1) merge, the reduction of Algorithm 6: per row, the best
 // (score, word) over the P split lists of length 1, in the strict order
-// higher score, then lower word.  Empty list slots hold scores below every
-// real one, and the split holding the row's maximum always lists it.
+// higher score, then lower word.  One wave per row: each lane scans the
+// splits lane, lane + 64, ..., then a wave-wide arg-best.  Empty list slots
+// hold scores below every real one, and the split holding the row's maximum
+// always lists it.
 __global__ __launch_bounds__(256) void k2_argmax(const int2* __restrict__ lists, int P, int N,
                                                  int32_t* __restrict__ tok, float* __restrict__ val) {
-  const int r = blockIdx.x * 256 + threadIdx.x;
-  if (r >= N) return;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= N) return;  // whole waves leave together
   float bv = -INFINITY;
   int bi = INT_MAX;
-  for (int p = 0; p < P; ++p) {
+  for (int p = lane; p < P; p += 64) {
     const int2 e = lists[(size_t)p * N + r];
     const float v = __int_as_float(e.x);
     if (better(v, e.y, bv, bi)) {
@@ -180,13 +183,24 @@ __global__ __launch_bounds__(256) void k2_argmax(const int2* __restrict__ lists,
       bi = e.y;
     }
   }
-  tok[r] = bi;
-  val[r] = bv;
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const float ov = __shfl_xor(bv, m, 64);
+    const int oi = __shfl_xor(bi, m, 64);
+    if (better(ov, oi, bv, bi)) {
+      bv = ov;
+      bi = oi;
+    }
+  }
+  if (lane == 0) {
+    tok[r] = bi;
+    val[r] = bv;
+  }
 }
 
 hipError_t launch_k2_argmax(const int2* lists, int P, int N, int32_t* tok, float* val, hipStream_t st) {
   if (N <= 0) return hipSuccess;
-  k2_argmax<<<dim3((N + 255) / 256), dim3(256), 0, st>>>(lists, P, N, tok, val);
+  k2_argmax<<<dim3((N + 3) / 4), dim3(256), 0, st>>>(lists, P, N, tok, val);
   return hipGetLastError();
 }
 
