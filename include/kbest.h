@@ -213,6 +213,56 @@ int kb_compact_batch(int S, int k, const uint8_t* alive, int32_t* keep_idx,
                      int32_t* kept_sentence, int32_t* new_S, void* stream);
 
 /*
+ * kb_beam_finish -- per-hypothesis end of sentence after a step (Section 2.1,
+ * Algorithm 2: every hypothesis that produced EOS leaves the batch; the
+ * sentence's beam shrinks with it, and the sentence is done when its beam is
+ * empty).  Run after kb_kbest_step(k) on the same S x k outputs, then
+ * kb_compact_batch on `alive`.  One step t of T (0 <= t < T):
+ *   token, parent, score   S x k outputs of kb_kbest_step (sorted per sentence).
+ *   sent_id                S int32: original id (0..S0-1) of each live sentence.
+ *   beam                   S int32, in/out: the sentence's beam size k_s <= k;
+ *                          only its first k_s continuations are taken.  On
+ *                          return, k_s minus the continuations that finished.
+ *   prev_keep, prev_hist_base
+ *                          the previous step's kb_compact_batch keep_idx and
+ *                          that step's hist_base: row i of this step's batch
+ *                          holds the hypothesis with history id
+ *                          prev_hist_base + prev_keep[i]; NULL at the first
+ *                          step (parents are the roots, history id -1).
+ *   hist_base              where this step's S*k history entries go:
+ *                          hist_token[hist_base + e] = token[e] and
+ *                          hist_parent[hist_base + e] = the parent's history id.
+ *   fin_*                  the finished store of each original sentence o,
+ *                          k slots at o*k: fin_count[o] used slots (in/out),
+ *                          fin_score (cumulative log-probability, EOS
+ *                          included), fin_len (tokens, EOS included = t + 1),
+ *                          fin_hist (history id of its last token).
+ *   alive                  S*k uint8 out: 1 for taken continuations that did
+ *                          not finish (the input of kb_compact_batch).
+ * A taken continuation finishes if its token is `eos`, or at the last step
+ * (t == T - 1) whatever it is.  Integer work except for copied scores: exact.
+ */
+int kb_beam_finish(int S, int k, int t, int T, int eos, const int32_t* token, const int32_t* parent,
+                   const float* score, const int32_t* sent_id, int32_t* beam, const int32_t* prev_keep,
+                   int prev_hist_base, int hist_base, int32_t* hist_token, int32_t* hist_parent,
+                   int32_t* fin_count, float* fin_score, int32_t* fin_len, int32_t* fin_hist,
+                   uint8_t* alive, void* stream);
+
+/*
+ * kb_beam_backtrace -- the translation of every sentence: among its finished
+ * hypotheses the one with the best length-normalised score
+ * fin_score / fin_len^alpha (alpha = 0: raw scores; ties: the one finished
+ * first), and its tokens, read back through the history.
+ *   out_tokens  S0 x T int32: the tokens in order, EOS included, then -1.
+ *   out_len     S0 int32 (0 for a sentence with nothing finished);
+ *   out_score   S0 float32, the raw score;  out_norm  S0 float32, normalised.
+ */
+int kb_beam_backtrace(int S0, int k, int T, float alpha, const int32_t* fin_count, const float* fin_score,
+                      const int32_t* fin_len, const int32_t* fin_hist, const int32_t* hist_token,
+                      const int32_t* hist_parent, int32_t* out_tokens, int32_t* out_len, float* out_score,
+                      float* out_norm, void* stream);
+
+/*
  * kb_gather_rows -- dst[i, :] = src[idx[i], :] for i < n, where
  * n = min(n_max, *n_dev) if n_dev is non-null, else n_max.  Rows are
  * row_bytes long (a multiple of 4); src, dst 4-byte aligned.  Moves the

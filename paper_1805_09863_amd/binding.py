@@ -39,6 +39,8 @@ SIGNATURES = {
     "kb_unfused_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I, _I]),
     "kb_kbest_step_unfused": (_I, [_I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ,
                                    _P, _I, _P]),
+    "kb_beam_finish": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "kb_beam_backtrace": (_I, [_I, _I, _I, ctypes.c_float, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "kb_compact_batch": (_I, [_I, _I, _P, _P, _P, _P, _P, _P, _P]),
     "kb_gather_rows": (_I, [_I, _P, _P, _P, _P, _SZ, _P]),
     # decoder stand-in of the synthetic decode loop (include/kbest_standin.h)
@@ -284,3 +286,30 @@ def standin_next_h(table: torch.Tensor, keep: torch.Tensor, sid: torch.Tensor, k
     _check(lib().kb_standin_next_h(n_max, _ptr(n_dev), k, T, t, _ptr(keep), _ptr(sid), _ptr(table), _ptr(out),
                                    row_bytes, _stream(stream)))
     return out
+
+
+# ---------------------------------------------------------------- per-hypothesis EOS
+def beam_finish(S: int, k: int, t: int, T: int, eos: int, token, parent, score, sent_id, beam, prev_keep,
+                prev_hist_base: int, hist_base: int, hist_token, hist_parent, fin: tuple, alive, stream=None):
+    """After a step: take each sentence's first beam[s] continuations, record the step's
+    history, move EOS (or last-step) continuations to the finished store ``fin`` =
+    (count, score, len, hist), shrink the beams and fill ``alive`` (include/kbest.h)."""
+    fc, fs, fl, fh = fin
+    _check(lib().kb_beam_finish(S, k, t, T, eos, _ptr(token), _ptr(parent), _ptr(score), _ptr(sent_id), _ptr(beam),
+                                _ptr(prev_keep), prev_hist_base, hist_base, _ptr(hist_token), _ptr(hist_parent),
+                                _ptr(fc), _ptr(fs), _ptr(fl), _ptr(fh), _ptr(alive), _stream(stream)))
+
+
+def beam_backtrace(S0: int, k: int, T: int, alpha: float, fin: tuple, hist_token, hist_parent, *, out=None,
+                   stream=None):
+    """Best finished hypothesis of every sentence by score / len**alpha, and its tokens:
+    returns (tokens[S0, T], len[S0], score[S0], normalised score[S0])."""
+    fc, fs, fl, fh = fin
+    dev = fc.device
+    if out is None:
+        out = (torch.empty((S0, T), dtype=torch.int32, device=dev), torch.empty(S0, dtype=torch.int32, device=dev),
+               torch.empty(S0, dtype=torch.float32, device=dev), torch.empty(S0, dtype=torch.float32, device=dev))
+    toks, ln, sc, nm = out
+    _check(lib().kb_beam_backtrace(S0, k, T, float(alpha), _ptr(fc), _ptr(fs), _ptr(fl), _ptr(fh), _ptr(hist_token),
+                                   _ptr(hist_parent), _ptr(toks), _ptr(ln), _ptr(sc), _ptr(nm), _stream(stream)))
+    return toks, ln, sc, nm

@@ -130,6 +130,17 @@ hipError_t launch_uf_kbest_rows(const float* p, int N, int V, int k, float2* sta
 hipError_t launch_uf_fused_rows(const float* x, const float* b, int N, int V, int k, float2* stats, int2* lists,
                                 hipStream_t st);
 
+// ---------------------------------------------------------------- per-hypothesis EOS
+hipError_t launch_beam_finish(int S, int k, int t, int T, int eos, const int32_t* token, const int32_t* parent,
+                              const float* score, const int32_t* sid, int32_t* beam, const int32_t* prev_keep,
+                              int prev_hist_base, int hist_base, int32_t* hist_token, int32_t* hist_parent,
+                              int32_t* fin_count, float* fin_score, int32_t* fin_len, int32_t* fin_hist,
+                              uint8_t* alive, hipStream_t st);
+hipError_t launch_beam_backtrace(int S0, int k, int T, float alpha, const int32_t* fin_count, const float* fin_score,
+                                 const int32_t* fin_len, const int32_t* fin_hist, const int32_t* hist_token,
+                                 const int32_t* hist_parent, int32_t* out_tokens, int32_t* out_len,
+                                 float* out_score, float* out_norm, hipStream_t st);
+
 // ---------------------------------------------------------------- decoder stand-in
 hipError_t launch_standin_alive(int S, int k, int t, const int32_t* sid, const int32_t* lengths, uint8_t* alive,
                                 hipStream_t st);

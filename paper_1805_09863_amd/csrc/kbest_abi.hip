@@ -418,6 +418,41 @@ int kb_argmax_step(int dtype, int N, int H, int V, const void* h, const void* W,
   return ok();
 }
 
+int kb_beam_finish(int S, int k, int t, int T, int eos, const int32_t* token, const int32_t* parent,
+                   const float* score, const int32_t* sent_id, int32_t* beam, const int32_t* prev_keep,
+                   int prev_hist_base, int hist_base, int32_t* hist_token, int32_t* hist_parent, int32_t* fin_count,
+                   float* fin_score, int32_t* fin_len, int32_t* fin_hist, uint8_t* alive, void* stream) {
+  if (S < 0 || k < 1 || k > KB_MAX_K || T < 1 || t < 0 || t >= T)
+    return fail(KB_ERR_INVALID_ARG, "S = %d, k = %d, t = %d, T = %d", S, k, t, T);
+  if (hist_base < 0 || prev_hist_base < 0 || (long long)hist_base + (long long)S * k > INT_MAX)
+    return fail(KB_ERR_INVALID_ARG, "history offsets out of range");
+  if (S == 0) return ok();
+  if (!token || !parent || !score || !sent_id || !beam || !hist_token || !hist_parent || !fin_count || !fin_score ||
+      !fin_len || !fin_hist || !alive)
+    return fail(KB_ERR_INVALID_ARG, "null pointer");
+  hipError_t e = kb::launch_beam_finish(S, k, t, T, eos, token, parent, score, sent_id, beam, prev_keep,
+                                        prev_hist_base, hist_base, hist_token, hist_parent, fin_count, fin_score,
+                                        fin_len, fin_hist, alive, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "beam finish kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int kb_beam_backtrace(int S0, int k, int T, float alpha, const int32_t* fin_count, const float* fin_score,
+                      const int32_t* fin_len, const int32_t* fin_hist, const int32_t* hist_token,
+                      const int32_t* hist_parent, int32_t* out_tokens, int32_t* out_len, float* out_score,
+                      float* out_norm, void* stream) {
+  if (S0 < 0 || k < 1 || k > KB_MAX_K || T < 1) return fail(KB_ERR_INVALID_ARG, "S0 = %d, k = %d, T = %d", S0, k, T);
+  if (S0 == 0) return ok();
+  if (!fin_count || !fin_score || !fin_len || !fin_hist || !hist_token || !hist_parent || !out_tokens || !out_len ||
+      !out_score || !out_norm)
+    return fail(KB_ERR_INVALID_ARG, "null pointer");
+  hipError_t e = kb::launch_beam_backtrace(S0, k, T, alpha, fin_count, fin_score, fin_len, fin_hist, hist_token,
+                                           hist_parent, out_tokens, out_len, out_score, out_norm,
+                                           reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "backtrace kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
 int kb_compact_batch(int S, int k, const uint8_t* alive, int32_t* keep_idx, int32_t* kept_count,
                      int32_t* new_sent_offsets, int32_t* kept_sentence, int32_t* new_S, void* stream) {
   if (S < 0) return fail(KB_ERR_INVALID_ARG, "S = %d < 0", S);

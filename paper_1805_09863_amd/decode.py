@@ -131,3 +131,109 @@ def decode_loop(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, lengths
     stats.steps = t
     stats.total_rows = sum(stats.rows)
     return stats
+
+
+@dataclass
+class BeamSearchResult:
+    tokens: torch.Tensor      # S0 x T int32: each sentence's translation, EOS included, then -1
+    length: torch.Tensor      # S0 int32
+    score: torch.Tensor       # S0 float32, cumulative log-probability
+    norm: torch.Tensor        # S0 float32, score / length**alpha
+    steps: int = 0
+    rows: list = field(default_factory=list)   # live rows decoded at each step
+
+
+def beam_search(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, k: int, T: int, eos: int, *,
+                alpha: float = 0.0, on_step: Optional[Callable] = None, stream=None) -> BeamSearchResult:
+    """Beam search with per-hypothesis end of sentence (Section 2.1, Algorithm 2).
+
+    ``h_table`` is (S0*T*k) x H on the device: row (s*T + t)*k + r is the state
+    of the hypothesis in slot r (its rank in the sentence's beam) of sentence s
+    at step t, the decoder stand-in.  Every sentence starts from one hypothesis
+    (slot 0, score 0) with a beam of k.  Each step: the output layer
+    (kb_kbest_step), kb_beam_finish (history, finished store, beam shrink),
+    kb_compact_batch, the gathers of the surviving scores, sentence ids and
+    beam sizes, and the stand-in's next states; then one wait for the two
+    counts.  A sentence ends when its beam is empty; step T - 1 finishes every
+    hypothesis left.  kb_beam_backtrace then picks each sentence's translation
+    by score / length**alpha.
+
+    ``on_step(t, state)`` is called after each step's kb_beam_finish with a
+    dict of the step's device tensors (before the batch is compacted).
+    """
+    dev = W.device
+    H, V = W.shape
+    S0 = h_table.shape[0] // (T * k)
+    if h_table.shape[0] != S0 * T * k or S0 == 0:
+        raise ValueError("h_table must hold S0 * T * k rows")
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    M0 = S0 * k
+    i32 = dict(dtype=torch.int32, device=dev)
+    dt = kbb._dtype_code(W)
+    # the plan (and so the workspace) depends on the row count, anything from 1 to S0*k
+    ws = kbb.workspace(max(kbb.kbest_workspace_bytes(dt, n, H, V, k, 1) for n in range(1, M0 + 1)), dev)
+    tok = torch.empty(M0, **i32)
+    par = torch.empty(M0, **i32)
+    sc = torch.empty(M0, dtype=torch.float32, device=dev)
+    h_cur = torch.empty((M0, H), dtype=h_table.dtype, device=dev)
+    alive = torch.empty(M0, dtype=torch.uint8, device=dev)
+    keep = [torch.empty(M0, **i32), torch.empty(M0, **i32)]
+    cnt = torch.empty(2, **i32)
+    noff = torch.empty(S0 + 1, **i32)
+    ksent = torch.empty(S0, **i32)
+    hist_tok = torch.empty(T * M0, **i32)
+    hist_par = torch.empty(T * M0, **i32)
+    fin = (torch.zeros(S0, **i32), torch.empty(M0, dtype=torch.float32, device=dev), torch.empty(M0, **i32),
+           torch.empty(M0, **i32))
+    sid, sid_nx = torch.arange(S0, **i32), torch.empty(S0, **i32)
+    beam, beam_nx = torch.full((S0,), k, **i32), torch.empty(S0, **i32)
+    prev, prev_nx = torch.zeros(M0, dtype=torch.float32, device=dev), torch.empty(M0, dtype=torch.float32, device=dev)
+    off = torch.arange(S0 + 1, **i32)                  # one row per sentence at the start
+    cnt_host = torch.empty(2, dtype=torch.int32, pin_memory=True)
+    ready = torch.cuda.Event()
+    # step 0's states: slot 0 of every sentence
+    kbb.standin_next_h(h_table, torch.arange(S0, **i32) * k, torch.arange(S0, **i32), k, T, 0, S0, out=h_cur,
+                       stream=stream)
+    out = BeamSearchResult(None, None, None, None)
+    S, N, t, cur, prev_base = S0, S0, 0, 0, 0
+    while S > 0 and t < T:
+        kbb.kbest_step(h_cur[:N], W, b, prev[:N], off[:S + 1], k, S=S,
+                       out=(tok[:S * k].view(S, k), par[:S * k].view(S, k), sc[:S * k].view(S, k)),
+                       ws=ws, stream=stream)
+        out.rows.append(N)
+        beam_before = beam[:S].clone() if on_step is not None else None
+        base = t * M0
+        kbb.beam_finish(S, k, t, T, eos, tok, par, sc, sid, beam, keep[1 - cur] if t > 0 else None, prev_base,
+                        base, hist_tok, hist_par, fin, alive, stream=stream)
+        if on_step is not None:
+            on_step(t, dict(h=h_cur[:N], prev=prev[:N], off=off[:S + 1], sid=sid[:S], beam_before=beam_before,
+                            beam_after=beam[:S], token=tok[:S * k].view(S, k), parent=par[:S * k].view(S, k),
+                            score=sc[:S * k].view(S, k), alive=alive[:S * k],
+                            prev_keep=keep[1 - cur][:N] if t > 0 else None, prev_base=prev_base, base=base,
+                            hist_token=hist_tok, hist_parent=hist_par, fin=fin, S=S, N=N))
+        kbb.compact_batch(alive[:S * k], S, k, out=(keep[cur], cnt[0:1], noff, ksent, cnt[1:2]), stream=stream)
+        cnt_host.copy_(cnt, non_blocking=True)
+        ready.record(stream)
+        kbb.gather_rows(sc[:S * k].view(S * k, 1), keep[cur], n_dev=cnt[0:1], n_max=S * k,
+                        out=prev_nx.view(M0, 1), stream=stream)
+        kbb.gather_rows(sid[:S].view(S, 1), ksent, n_dev=cnt[1:2], n_max=S, out=sid_nx.view(S0, 1), stream=stream)
+        kbb.gather_rows(beam[:S].view(S, 1), ksent, n_dev=cnt[1:2], n_max=S, out=beam_nx.view(S0, 1),
+                        stream=stream)
+        if t + 1 < T:
+            kbb.standin_next_h(h_table, keep[cur], sid, k, T, t + 1, S * k, n_dev=cnt[0:1], out=h_cur, stream=stream)
+        ready.synchronize()                            # the step's one host sync
+        N, S = (int(x) for x in cnt_host.tolist())
+        prev, prev_nx = prev_nx, prev
+        sid, sid_nx = sid_nx, sid
+        beam, beam_nx = beam_nx, beam
+        off, noff = noff, off
+        prev_base = base
+        cur = 1 - cur
+        t += 1
+    out.tokens, out.length, out.score, out.norm = kbb.beam_backtrace(S0, k, T, alpha, fin, hist_tok, hist_par,
+                                                                     stream=stream)
+    out.steps = t
+    out.fin = fin
+    out.hist = (hist_tok, hist_par)
+    return out

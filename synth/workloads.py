@@ -271,3 +271,51 @@ def make_loop_workload(seed: Optional[int] = None, S: Optional[int] = None, V: O
     prev0 = g.uniform(-5.0, 0.0, size=S * c["beam"]).astype(np.float32)
     return LoopWorkload(S=S, beam=c["beam"], H=H, V=V, k=c["k"], T=T, lengths=lengths,
                         W=W, b=b, prev0=prev0, seed=sd)
+
+
+# --------------------------------------------------------------------------
+# natural end of sentence: a decoder stand-in whose EOS score rises with the step
+# --------------------------------------------------------------------------
+@dataclasses.dataclass
+class EosWorkload:
+    S: int
+    k: int
+    H: int
+    V: int
+    T: int
+    eos: int
+    lengths: np.ndarray   # S int32: the step around which each sentence's EOS score overtakes
+    W: np.ndarray         # H x V bf16 bits
+    b: np.ndarray         # V float32
+    gamma: float
+    seed: int
+
+    def h_rows(self, s: int, t: int) -> np.ndarray:
+        """bf16 bits of the k states of sentence s at step t: N(0, 1) noise plus
+        gamma * (t - L_s) along the direction that raises the EOS score by
+        exactly that much (W[:, eos] / |W[:, eos]|^2), so hypotheses end around
+        their sentence's length, each at its own step."""
+        g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([self.seed, 11, s, t])))
+        x = g.standard_normal((self.k, self.H))
+        w = bf16_bits_to_f32(self.W[:, self.eos]).astype(np.float64)
+        x = x + self.gamma * (t - float(self.lengths[s])) * (w / np.dot(w, w))[None, :]
+        return f32_to_bf16_bits(x.astype(np.float32))
+
+    def h_table(self) -> np.ndarray:
+        """All states as a [S, T, k, H] uint16 array (bf16 bits)."""
+        out = np.empty((self.S, self.T, self.k, self.H), dtype=np.uint16)
+        for s in range(self.S):
+            for t in range(self.T):
+                out[s, t] = self.h_rows(s, t)
+        return out
+
+
+def make_eos_workload(S: int = 24, k: int = 4, H: int = 128, V: int = 500, T: int = 14, Lmin: int = 2,
+                      Lmax: int = 9, eos: int = 3, gamma: float = 3.0, seed: Optional[int] = None) -> EosWorkload:
+    """Weights, bias and drawn lengths for a beam search with natural EOS."""
+    sd = SEED_BASE + 50 if seed is None else seed
+    g = np.random.Generator(np.random.PCG64(sd))
+    W = f32_to_bf16_bits(_normal(g, (H, V), 1.0 / np.sqrt(H)))
+    b = g.uniform(-0.1, 0.1, V).astype(np.float32)
+    lengths = g.integers(Lmin, Lmax + 1, S).astype(np.int32)
+    return EosWorkload(S, k, H, V, T, eos, lengths, W, b, gamma, sd)
