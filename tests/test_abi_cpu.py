@@ -147,14 +147,14 @@ def test_beam_argument_checks():
     P = [FAKE] * 3
     # kb_beam_finish(S, k, t, T, eos, token, parent, score, sid, beam, prev_keep, prev_base, base, ...)
     fin = [FAKE] * 4
-    ok_tail = [FAKE, FAKE, FAKE, None, 0, 0, FAKE, FAKE] + fin + [FAKE, None]
+    ok_tail = [FAKE, FAKE, None, 0, 0, FAKE, FAKE] + fin + [FAKE, None]   # sid, beam, prev_keep, bases, ...
     assert L.kb_beam_finish(0, 4, 0, 10, 3, *P, *ok_tail) == KB_OK                            # empty batch
     assert L.kb_beam_finish(5, 0, 0, 10, 3, *P, *ok_tail) == KB_ERR_INVALID_ARG               # k
     assert L.kb_beam_finish(5, 17, 0, 10, 3, *P, *ok_tail) == KB_ERR_INVALID_ARG              # k > 16
     assert L.kb_beam_finish(5, 4, 10, 10, 3, *P, *ok_tail) == KB_ERR_INVALID_ARG              # t >= T
-    bad = [FAKE, FAKE, FAKE, None, 0, 0, None, FAKE] + fin + [FAKE, None]
+    bad = [FAKE, FAKE, None, 0, 0, None, FAKE] + fin + [FAKE, None]
     assert L.kb_beam_finish(5, 4, 0, 10, 3, *P, *bad) == KB_ERR_INVALID_ARG                   # null history
-    neg = [FAKE, FAKE, FAKE, None, 0, -1, FAKE, FAKE] + fin + [FAKE, None]
+    neg = [FAKE, FAKE, None, 0, -1, FAKE, FAKE] + fin + [FAKE, None]
     assert L.kb_beam_finish(5, 4, 0, 10, 3, *P, *neg) == KB_ERR_INVALID_ARG                   # base < 0
     out = [FAKE] * 4
     assert L.kb_beam_backtrace(0, 4, 10, 1.0, *fin, FAKE, FAKE, *out, None) == KB_OK
