@@ -321,6 +321,35 @@ def sweep_bench(torch, np, kb):
             f"naive {r['naive']['seconds'] * 1e3:.2f} ms")
         by_s.append(r)
     out["decode_vs_sentences"] = by_s
+    # (4) beam search with natural end of sentence (per-hypothesis EOS, beam shrink,
+    # length-normalised choice, backtrace), 1280 sentences at beam 5
+    from paper_1805_09863_amd.decode import beam_search
+    eos, T2 = 3, 80
+    gen = torch.Generator(device="cuda").manual_seed(wl.SEED_BASE + 6)
+    Ls = torch.randint(5, 61, (S0,), generator=gen, device="cuda").float()
+    w = W[:, eos].float()
+    u = (w / (w @ w)).to(torch.bfloat16)
+    tab = torch.empty((S0 * T2 * beam, H), dtype=torch.bfloat16, device="cuda")
+    step_of_row = (torch.arange(T2, device="cuda").repeat_interleave(beam)).float()   # t of rows (s, t, r)
+    for s0 in range(0, S0, 64):                       # the stand-in's states, drawn on the device
+        n = min(64, S0 - s0)
+        x = torch.randn((n, T2 * beam, H), generator=gen, device="cuda")
+        ramp = 3.0 * (step_of_row[None, :] - Ls[s0:s0 + n, None])
+        tab[s0 * T2 * beam:(s0 + n) * T2 * beam] = (x + ramp[:, :, None] * u.float()[None, None, :]).reshape(
+            -1, H).to(torch.bfloat16)
+    beam_search(tab, W, b, beam, T2, eos, alpha=1.0)   # warm-up
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    r = beam_search(tab, W, b, beam, T2, eos, alpha=1.0)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ln = r.length.float()
+    out["beam_search_natural_eos_1280"] = {
+        "seconds": dt, "steps": r.steps, "live_rows": sum(r.rows), "live_hyps_per_s": sum(r.rows) / dt,
+        "sentences_per_s": S0 / dt, "mean_length": float(ln.mean()), "max_length": int(ln.max()),
+        "setup": f"{S0} sentences, beam {beam}, EOS score rising 3 per step past a length ~U{{5..60}}, "
+                 f"cap T={T2}, alpha=1"}
+    log(f"beam search, natural EOS: {dt * 1e3:.2f} ms, {r.steps} steps, {sum(r.rows)} live rows")
     return out
 
 
