@@ -144,6 +144,34 @@ def test_config_v90k_sampled(kb):
     say(f"  max score err {rep.max_score_err:.2e}, {rep.n_checked_idx} exact ranks")
 
 
+@pytest.mark.parametrize("k,N,H", [(16, 4096, 1024), (12, 1280, 2048)])
+def test_large_shapes_sampled(kb, k, N, H):
+    # the largest k at more rows than the V=90k workload, and a longer state
+    # (H = 2048: 64 stages per word tile), V = 90,000 with the Zipf bias;
+    # the oracle checks sampled sentences
+    inp = wl.make_step(H=H, V=90000, k=k, S=N // k if N % k == 0 else N // 16, beam=k if N % k == 0 else 16,
+                       dtype="bf16", seed=7000 + k, bias="zipf", name=f"large_k{k}_H{H}")
+    say(f"large shape: N={inp.N} H={H} V=90000 k={k}")
+    out = run_step(kb, inp, row_lse=True)
+    sents = sorted(set(np.random.default_rng(k).choice(inp.S, 6, replace=False).tolist()) | {0, inp.S - 1})
+    rep, _ = check(inp, out, sentences=sents)
+    say(f"  max score err {rep.max_score_err:.2e}, {rep.n_checked_idx} exact ranks")
+
+
+def test_empty_batch_is_a_no_op(kb):
+    h = torch.empty((0, 128), dtype=torch.bfloat16, device="cuda")
+    W = torch.zeros((128, 1000), dtype=torch.bfloat16, device="cuda")
+    b = torch.zeros(1000, dtype=torch.float32, device="cuda")
+    prev = torch.empty(0, dtype=torch.float32, device="cuda")
+    off = torch.zeros(1, dtype=torch.int32, device="cuda")
+    tok, par, sc = kb.kbest_step(h, W, b, prev, off, 5, S=0, ws=kb.workspace(1))
+    torch.cuda.synchronize()
+    assert tok.shape == (0, 5) and sc.numel() == 0
+    keep, kept, noff, ksent, nS = kb.compact_batch(torch.empty(0, dtype=torch.uint8, device="cuda"), 0, 5)
+    torch.cuda.synchronize()
+    assert int(kept.item()) == 0 and int(nS.item()) == 0 and int(noff[0].item()) == 0
+
+
 def test_deterministic_and_workspace_poison(kb):
     inp = wl.make_step(H=256, V=12000, k=12, S=30, beam=12, dtype="bf16", seed=55, name="det")
     need = kb.kbest_workspace_bytes(kb.KB_BF16, inp.N, inp.H, inp.V, inp.k, inp.S)
