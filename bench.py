@@ -238,8 +238,35 @@ def ablation_bench(torch, np, kb, reps: int = 10):
             g[name + "_ms"] = e0.elapsed_time(e1) / (reps * 2)
         log(f"greedy N={N}: k=1 step {g['kbest_k1_ms']:.3f} ms, argmax {g['greedy_argmax_ms']:.3f} ms")
         greedy.append(g)
+    # the half-precision comparison (the paper's tensor-core table): the same step
+    # with float32 h and W (fp32 MFMA) against bf16 storage (bf16 MFMA), beams 1 and 9
+    prec = []
+    W32 = torch.from_numpy(wl.bf16_bits_to_f32(big.W)).cuda()
+    for beam in (1, 9):
+        N, k = S * beam, beam
+        hb = torch.from_numpy(np.ascontiguousarray(big.h[:N]).view(np.int16)).view(torch.bfloat16).cuda()
+        h32 = hb.float()
+        prev = torch.from_numpy(np.ascontiguousarray(big.prev[:N])).cuda()
+        off = torch.from_numpy(wl.uniform_offsets(S, beam)).cuda()
+        out = tuple(torch.empty((S, k), dtype=t, device="cuda") for t in (torch.int32, torch.int32, torch.float32))
+        g = {"beam": beam, "N": N}
+        for name, hh, WW, dt in (("float32", h32, W32, kb.KB_F32), ("bf16", hb, W, kb.KB_BF16)):
+            ws = kb.workspace(kb.kbest_workspace_bytes(dt, N, H, V, k, S))
+            for _ in range(2):
+                kb.kbest_step(hh, WW, b, prev, off, k, out=out, ws=ws)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(reps):
+                kb.kbest_step(hh, WW, b, prev, off, k, out=out, ws=ws)
+            e1.record()
+            torch.cuda.synchronize()
+            g[name + "_ms"] = e0.elapsed_time(e1) / reps
+        log(f"precision beam {beam}: float32 {g['float32_ms']:.3f} ms, bf16 {g['bf16_ms']:.3f} ms")
+        prec.append(g)
+    del W32
     return {"workload": f"S={S} sentences x beam 1/3/9 (k = beam), H={H}, V={V}, bf16, Zipf bias",
-            "reps": reps, "rows": rows, "greedy_beam1": greedy}
+            "reps": reps, "rows": rows, "greedy_beam1": greedy, "precision": prec}
 
 
 def sweep_bench(torch, np, kb):
