@@ -1,145 +1,268 @@
 // K2: merge the vocabulary splits of every row, then the rows of every sentence.
 //
-// One workgroup per sentence.  For each of its rows (one wave per row):
+// One workgroup per sentence, W waves (W <= 16, as many as the staged lists
+// fit in LDS); the sentence's rows are taken W at a time, one per wave:
+//   * the row's P split lists are staged in LDS, all loads in flight, and its
+//     P split statistics held in registers;
 //   * LSE = M + ln(sum_p s_p * exp(m_p - M)) over the P split partials -- the
 //     rescaling identity of Algorithm 4 applied between shards, the reduction
 //     step of Algorithm 6 extended from (max, best) to softmax statistics;
-//   * the row's k best words: k rounds of a wave-wide arg-best over the heads
-//     of the P sorted split lists (strict total order: higher score, then
-//     lower word);
-//   * candidate score = prev + x - LSE.
-// Rows are taken in chunks; each chunk's candidates and the running k best of
-// the sentence are ranked by (score desc, flat index asc), flat index being
-// (row - first row) * V + word, and the first k are kept.  Because the score
-// adds a per-row constant to x, a sentence's k best lie in the union of its
-// rows' k best, so nothing outside these candidates can be selected.
+//   * the row's best words: rounds of a wave-wide arg-best (DPP) over the
+//     heads of the P sorted split lists (strict total order: higher score,
+//     then lower word).  Each lane keeps its lists' heads and the entries
+//     after them in registers, so a round reads no LDS on its critical path.
+//     The rounds stop once a score (prev + x - LSE) falls below the sentence's
+//     k-th best so far: the row's later entries are worse still;
+//   * the running k best of the sentence and the chunk's candidates are ranked
+//     by (score desc, flat index asc), flat index being
+//     (row - first row) * V + word, one thread per candidate, and the first k
+//     kept.  Because the score adds a per-row constant to x, a sentence's k
+//     best lie in the union of its rows' k best, so nothing outside these
+//     candidates can be selected.
 #include "kb_common.hpp"
 
 namespace kb {
 
-constexpr int K2_RC = 16;   // rows per chunk
-constexpr int K2_LPL = 4;   // split lists per lane: P <= 256
-constexpr int K2_C = K2_RC * 16 + 16;
+constexpr int K2_MAXW = 16;                  // waves per workgroup: rows merged at once
+constexpr int K2_LPL = 4;                    // split lists per lane: P <= 256
+constexpr int K2_LS = 16;                    // LDS slots per staged split list (k <= 16)
+constexpr int K2_C = K2_MAXW * 16 + 16 + 2;  // running best + one chunk (+ pad to pairs)
+constexpr int kNegInfBits = (int)0xff800000;  // -inf: the score of an empty entry (word INT_MAX)
+static_assert(K2_C % 2 == 0, "candidate keys are read in pairs");
 
-struct Cand {
-  float s;
-  int flat;
-};
-
-__device__ __forceinline__ bool cbetter(float a, int fa, float b, int fb) { return a > b || (a == b && fa < fb); }
+// Wave-wide reductions from DPP moves within each row of 16 lanes (quad
+// xor 1, quad xor 2, half-row mirror, row mirror), then the four row results
+// read out (v_readlane): no LDS permutes on the merge's critical path.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+__device__ __forceinline__ float lane_f(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
 
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
-  return v;
+  v = fmaxf(v, dpp_f<kDppXor1>(v));
+  v = fmaxf(v, dpp_f<kDppXor2>(v));
+  v = fmaxf(v, dpp_f<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp_f<kDppMirror>(v));
+  return fmaxf(fmaxf(lane_f(v, 0), lane_f(v, 16)), fmaxf(lane_f(v, 32), lane_f(v, 48)));
 }
 __device__ __forceinline__ float wave_sum(float v) {
+  v += dpp_f<kDppXor1>(v);
+  v += dpp_f<kDppXor2>(v);
+  v += dpp_f<kDppHalfMirror>(v);
+  v += dpp_f<kDppMirror>(v);
+  return (lane_f(v, 0) + lane_f(v, 16)) + (lane_f(v, 32) + lane_f(v, 48));
+}
+// the best (score, word) of the wave under better(); every lane gets it
+template <int CTRL>
+__device__ __forceinline__ void argbest_step(float& v, int& i) {
+  const float ov = dpp_f<CTRL>(v);
+  const int oi = dpp_i<CTRL>(i);
+  if (better(ov, oi, v, i)) {
+    v = ov;
+    i = oi;
+  }
+}
+__device__ __forceinline__ void wave_argbest(float& v, int& i) {
+  argbest_step<kDppXor1>(v, i);
+  argbest_step<kDppXor2>(v, i);
+  argbest_step<kDppHalfMirror>(v, i);
+  argbest_step<kDppMirror>(v, i);
+  float bv = lane_f(v, 0);
+  int bi = __builtin_amdgcn_readlane(i, 0);
 #pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
-  return v;
+  for (int l = 16; l < 64; l += 16) {
+    const float ov = lane_f(v, l);
+    const int oi = __builtin_amdgcn_readlane(i, l);
+    if (better(ov, oi, bv, bi)) {
+      bv = ov;
+      bi = oi;
+    }
+  }
+  v = bv;
+  i = bi;
 }
 
-__global__ __launch_bounds__(256) void k2_merge(K2Args a) {
-  __shared__ float c_s[K2_C];
-  __shared__ int c_f[K2_C];
+// A candidate as one 64-bit key whose unsigned order is the merge order:
+// the score mapped to an order-preserving integer (-0 taken as +0, as the
+// float comparison does) above the complement of the flat index, so a higher
+// score, then a lower flat index, gives the larger key.
+__device__ __forceinline__ uint64_t cand_key(float score, int flat) {
+  const uint32_t u = (uint32_t)__float_as_int(score + 0.f);
+  const uint32_t o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((uint64_t)o << 32) | (uint32_t)~(uint32_t)flat;
+}
+__device__ __forceinline__ float key_score(uint64_t key) {
+  const uint32_t o = (uint32_t)(key >> 32);
+  return __int_as_float((int)((o & 0x80000000u) ? (o & 0x7fffffffu) : ~o));
+}
+
+template <int NQ>  // split lists per lane: P <= 64 * NQ
+__global__ __launch_bounds__(1024) void k2_merge(K2Args a) {
+  __shared__ __align__(16) uint64_t key[K2_C];  // read two at a time when ranked
   __shared__ int c_t[K2_C];
   __shared__ int c_p[K2_C];
-  __shared__ float n_s[16];
-  __shared__ int n_f[16], n_t[16], n_p[16];
+  __shared__ uint64_t n_key[16];
+  __shared__ int n_t[16], n_p[16];
+  // one list of empty entries, then per wave one row's P lists of K2_LS slots
+  extern __shared__ int2 lists_dyn[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int W = blockDim.x >> 6;
   const int s = blockIdx.x;
-  const int k = a.k;
+  const int k = a.k, P = a.P;
   const int r0 = a.off[s], r1 = a.off[s + 1];
 
-  // running best k of the sentence lives in slots [0, k)
+  if (tid < K2_LS) lists_dyn[tid] = make_int2(kNegInfBits, INT_MAX);
+  // running best k of the sentence lives in slots [0, k); empty slots hold
+  // distinct keys below every real candidate
   if (tid < k) {
-    c_s[tid] = -INFINITY;
-    c_f[tid] = INT_MAX - tid;  // distinct keys for empty slots
+    key[tid] = cand_key(-INFINITY, INT_MAX - tid);
     c_t[tid] = -1;
     c_p[tid] = -1;
   }
+  const int wbase = K2_LS + wave * P * K2_LS;  // this wave's lists in lists_dyn
+  int lidx[NQ];  // each lane's lists, or the empty list where it has none
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int p = lane + 64 * q;
+    lidx[q] = p < P ? wbase + p * K2_LS : 0;
+  }
 
-  for (int cr0 = r0; cr0 < r1; cr0 += K2_RC) {
-    const int nrows = min(K2_RC, r1 - cr0);
-    for (int ri = wave; ri < nrows; ri += 4) {
-      const int r = cr0 + ri;
+  for (int cr0 = r0; cr0 < r1; cr0 += W) {
+    const int nrows = min(W, r1 - cr0);
+    const int ri = wave;
+    const bool active = ri < nrows;
+    const int r = cr0 + ri;
+    float2 st[NQ];
+    if (active) {
+      // lane = 16 * g + j stages entry j of lists p0 + g, p0 + 4 + g, ...
+      // (slots j >= k get empty entries): four loads in flight per lane
+      // before the first LDS write
+      const int j = lane & 15, g = lane >> 4;
+      for (int p0 = 0; p0 < P; p0 += 16) {
+        int2 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int p = p0 + 4 * u + g;
+          v[u] = make_int2(kNegInfBits, INT_MAX);
+          if (p < P && j < k) v[u] = a.lists[((size_t)p * a.N + r) * k + j];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int p = p0 + 4 * u + g;
+          if (p < P) lists_dyn[wbase + p * K2_LS + j] = v[u];
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int p = lane + 64 * q;
+        st[q] = p < P ? a.stats[(size_t)p * a.N + r] : make_float2(kStatInit, 0.f);
+      }
+    }
+    __syncthreads();  // the staged lists are visible; the running best is settled
+    uint64_t my_key = cand_key(-INFINITY, INT_MAX - (k + ri * k + lane));
+    int my_t = -1;
+    if (active) {
       float M = kStatInit;
-      for (int p = lane; p < a.P; p += 64) M = fmaxf(M, a.stats[(size_t)p * a.N + r].x);
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) M = fmaxf(M, st[q].x);
       M = wave_max(M);
       float S = 0.f;
-      for (int p = lane; p < a.P; p += 64) {
-        const float2 st = a.stats[(size_t)p * a.N + r];
-        S += st.y * __expf(st.x - M);
-      }
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) S += st[q].y * __expf(st[q].x - M);
       S = wave_sum(S);
       const float lse = M + __logf(S);
       if (a.row_lse != nullptr && lane == 0) a.row_lse[r] = lse;
       const float base = a.prev[r] - lse;
+      const float kth = key_score(key[k - 1]);  // running k-th best (-inf before the first chunk)
 
-      int ptr[K2_LPL];
+      // per list of this lane: the head (entry ptr) and the entry after it
+      float hv[NQ], nv[NQ];
+      int hi[NQ], ni[NQ], ptr[NQ];
 #pragma unroll
-      for (int q = 0; q < K2_LPL; ++q) ptr[q] = 0;
-      for (int j = 0; j < k; ++j) {
+      for (int q = 0; q < NQ; ++q) {
+        const int2 h = lists_dyn[lidx[q]];
+        const int2 n = lists_dyn[lidx[q] + 1];
+        hv[q] = __int_as_float(h.x);
+        hi[q] = h.y;
+        nv[q] = __int_as_float(n.x);
+        ni[q] = n.y;
+        ptr[q] = 0;
+      }
+      for (int jr = 0; jr < k; ++jr) {
         float bv = -INFINITY;
         int bi = INT_MAX, bq = -1;
 #pragma unroll
-        for (int q = 0; q < K2_LPL; ++q) {
-          const int p = lane + 64 * q;
-          if (p < a.P && ptr[q] < k) {
-            const int2 e = a.lists[((size_t)p * a.N + r) * k + ptr[q]];
-            const float v = __int_as_float(e.x);
-            if (better(v, e.y, bv, bi)) {
-              bv = v;
-              bi = e.y;
-              bq = q;
-            }
+        for (int q = 0; q < NQ; ++q)
+          if (better(hv[q], hi[q], bv, bi)) {
+            bv = hv[q];
+            bi = hi[q];
+            bq = q;
           }
-        }
         float wv = bv;
         int wi = bi;
-#pragma unroll
-        for (int m = 32; m >= 1; m >>= 1) {
-          const float ov = __shfl_xor(wv, m, 64);
-          const int oi = __shfl_xor(wi, m, 64);
-          if (better(ov, oi, wv, wi)) {
-            wv = ov;
-            wi = oi;
-          }
+        wave_argbest(wv, wi);
+        // the row's later entries are worse still: once this one scores below
+        // the sentence's k-th best of the rows ranked so far, none can enter
+        if (wv + base < kth) break;
+        if (lane == jr && wv > -INFINITY) {
+          my_key = cand_key(wv + base, (r - r0) * a.V + wi);
+          my_t = wi;
         }
-        // the lane whose head won advances that list (entries are unique)
+        // the lane whose head won advances that list (entries are unique);
+        // every lane then reloads the entry after its head, so the read is
+        // waited for only at the next advance.  A list advances at most k
+        // times, and its head is compared only while rounds remain, so the
+        // clamped read past the last slot is never used.
 #pragma unroll
-        for (int q = 0; q < K2_LPL; ++q)
-          if (bq == q && bv == wv && bi == wi) ++ptr[q];
-        if (lane == 0) {
-          const int slot = k + ri * k + j;
-          const bool valid = wv > -INFINITY;
-          c_s[slot] = valid ? (wv + base) : -INFINITY;
-          c_f[slot] = valid ? (r - r0) * a.V + wi : INT_MAX - slot;
-          c_t[slot] = wi;
-          c_p[slot] = r;
+        for (int q = 0; q < NQ; ++q) {
+          const bool adv = bq == q && bv == wv && bi == wi;
+          hv[q] = adv ? nv[q] : hv[q];
+          hi[q] = adv ? ni[q] : hi[q];
+          ptr[q] += adv ? 1 : 0;
+          const int2 n = lists_dyn[lidx[q] + min(ptr[q] + 1, K2_LS - 1)];
+          nv[q] = __int_as_float(n.x);
+          ni[q] = n.y;
         }
       }
     }
+    const int C = k + nrows * k;
+    if (active && lane < k) {
+      const int slot = k + ri * k + lane;
+      key[slot] = my_key;
+      c_t[slot] = my_t;
+      c_p[slot] = r;
+    }
+    if (tid == 0 && (C & 1)) key[C] = 0;  // pairs: a pad below every key
     __syncthreads();
     // rank every candidate (running best + this chunk) and keep the first k
-    const int C = k + nrows * k;
-    for (int c = tid; c < C; c += 256) {
-      const float sc = c_s[c];
-      const int fl = c_f[c];
+    if (tid < C) {
+      const uint64_t me = key[tid];
+      const ulonglong2* kp = reinterpret_cast<const ulonglong2*>(key);
       int rank = 0;
-      for (int o = 0; o < C; ++o) rank += cbetter(c_s[o], c_f[o], sc, fl) ? 1 : 0;
+      const int C2 = (C + 1) >> 1;
+#pragma unroll 4
+      for (int o = 0; o < C2; ++o) {
+        const ulonglong2 q = kp[o];
+        rank += (q.x > me ? 1 : 0) + (q.y > me ? 1 : 0);
+      }
       if (rank < k) {
-        n_s[rank] = sc;
-        n_f[rank] = fl;
-        n_t[rank] = c_t[c];
-        n_p[rank] = c_p[c];
+        n_key[rank] = me;
+        n_t[rank] = c_t[tid];
+        n_p[rank] = c_p[tid];
       }
     }
     __syncthreads();
     if (tid < k) {
-      c_s[tid] = n_s[tid];
-      c_f[tid] = n_f[tid];
+      key[tid] = n_key[tid];
       c_t[tid] = n_t[tid];
       c_p[tid] = n_p[tid];
     }
@@ -148,7 +271,7 @@ __global__ __launch_bounds__(256) void k2_merge(K2Args a) {
   if (tid < k) {
     a.tok[s * k + tid] = c_t[tid];
     a.par[s * k + tid] = c_p[tid];
-    a.score[s * k + tid] = c_s[tid];
+    a.score[s * k + tid] = key_score(key[tid]);
   }
 }
 
@@ -183,15 +306,7 @@ __global__ __launch_bounds__(256) void k2_argmax(const int2* __restrict__ lists,
       bi = e.y;
     }
   }
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) {
-    const float ov = __shfl_xor(bv, m, 64);
-    const int oi = __shfl_xor(bi, m, 64);
-    if (better(ov, oi, bv, bi)) {
-      bv = ov;
-      bi = oi;
-    }
-  }
+  wave_argbest(bv, bi);
   if (lane == 0) {
     tok[r] = bi;
     val[r] = bv;
@@ -204,10 +319,31 @@ hipError_t launch_k2_argmax(const int2* lists, int P, int N, int32_t* tok, float
   return hipGetLastError();
 }
 
-hipError_t launch_k2(const K2Args& a, hipStream_t st) {
-  if (a.P > 64 * K2_LPL || a.k > 16) return hipErrorInvalidValue;
-  k2_merge<<<dim3(a.S), dim3(256), 0, st>>>(a);
+template <int NQ>
+static hipError_t launch_k2_nq(const K2Args& a, hipStream_t st) {
+  // as many waves (rows at once) as the staged lists fit in 144 KB of LDS
+  // (the kernel's static LDS is under 4 KB): 16 up to P = 72, 4 at P = 256
+  const size_t per_wave = (size_t)a.P * K2_LS * sizeof(int2);
+  const int W = (int)std::min<size_t>(K2_MAXW, (144 * 1024) / per_wave);
+  const size_t lds = (size_t)K2_LS * sizeof(int2) + (size_t)W * per_wave;
+  if (lds > 48 * 1024) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k2_merge<NQ>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  k2_merge<NQ><<<dim3(a.S), dim3(64 * W), lds, st>>>(a);
   return hipGetLastError();
+}
+
+hipError_t launch_k2(const K2Args& a, hipStream_t st) {
+  if (a.P < 1 || a.P > 64 * K2_LPL || a.k < 1 || a.k > K2_LS) return hipErrorInvalidValue;
+  if (a.S <= 0) return hipSuccess;
+  switch ((a.P + 63) / 64) {
+    case 1: return launch_k2_nq<1>(a, st);
+    case 2: return launch_k2_nq<2>(a, st);
+    case 3: return launch_k2_nq<3>(a, st);
+    default: return launch_k2_nq<4>(a, st);
+  }
 }
 
 }  // namespace kb

@@ -37,6 +37,8 @@ SMALL = [
     ([5] * 80, 512, 1000, 5, "bf16"),          # 400 rows
     ([9] * 30, 128, 20000, 9, "bf16"),
     ([1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15, 16, 17], 64, 5000, 7, "f32"),
+    ([40, 3], 64, 60000, 16, "bf16"),          # many splits per row, a sentence of 40 rows
+    ([20, 17, 1], 64, 30000, 13, "f32"),       # sentences longer than one merge chunk
 ]
 
 
