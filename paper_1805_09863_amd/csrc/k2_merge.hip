@@ -144,19 +144,19 @@ __global__ __launch_bounds__(1024) void k2_merge(K2Args a) {
     float2 st[NQ];
     if (active) {
       // lane = 16 * g + j stages entry j of lists p0 + g, p0 + 4 + g, ...
-      // (slots j >= k get empty entries): four loads in flight per lane
-      // before the first LDS write
+      // (slots j >= k get empty entries): 32 lists per pass, eight loads in
+      // flight per lane before the first LDS write
       const int j = lane & 15, g = lane >> 4;
-      for (int p0 = 0; p0 < P; p0 += 16) {
-        int2 v[4];
+      for (int p0 = 0; p0 < P; p0 += 32) {
+        int2 v[8];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < 8; ++u) {
           const int p = p0 + 4 * u + g;
           v[u] = make_int2(kNegInfBits, INT_MAX);
           if (p < P && j < k) v[u] = a.lists[((size_t)p * a.N + r) * k + j];
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < 8; ++u) {
           const int p = p0 + 4 * u + g;
           if (p < P) lists_dyn[wbase + p * K2_LS + j] = v[u];
         }

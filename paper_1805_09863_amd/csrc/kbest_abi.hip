@@ -20,6 +20,12 @@ hipError_t launch_k1_reg_f32_L32(int kc, dim3 grid, const K1Args& a, hipStream_t
 hipError_t launch_k1_dma_L256(int kc, dim3 grid, const K1Args& a, hipStream_t st);
 hipError_t launch_k1_dma_L128(int kc, dim3 grid, const K1Args& a, hipStream_t st);
 hipError_t launch_k1_dma_L32(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_reg_bf16_L32M(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_reg_bf16_L32S(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_reg_f32_L32M(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_reg_f32_L32S(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_dma_L32M(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_dma_L32S(int kc, dim3 grid, const K1Args& a, hipStream_t st);
 hipError_t launch_k1_wide(int kc, dim3 grid, const K1Args& a, hipStream_t st);
 
 hipError_t launch_k1(int bf16, int dma, int layout, int kc, dim3 grid, const K1Args& a, hipStream_t st) {
@@ -28,6 +34,8 @@ hipError_t launch_k1(int bf16, int dma, int layout, int kc, dim3 grid, const K1A
       case K1_W256: return launch_k1_wide(kc, grid, a, st);
       case K1_L256: return launch_k1_dma_L256(kc, grid, a, st);
       case K1_L128: return launch_k1_dma_L128(kc, grid, a, st);
+      case K1_L32M: return launch_k1_dma_L32M(kc, grid, a, st);
+      case K1_L32S: return launch_k1_dma_L32S(kc, grid, a, st);
       default: return launch_k1_dma_L32(kc, grid, a, st);
     }
   }
@@ -35,12 +43,16 @@ hipError_t launch_k1(int bf16, int dma, int layout, int kc, dim3 grid, const K1A
     switch (layout) {
       case K1_L256: return launch_k1_reg_bf16_L256(kc, grid, a, st);
       case K1_L128: return launch_k1_reg_bf16_L128(kc, grid, a, st);
+      case K1_L32M: return launch_k1_reg_bf16_L32M(kc, grid, a, st);
+      case K1_L32S: return launch_k1_reg_bf16_L32S(kc, grid, a, st);
       default: return launch_k1_reg_bf16_L32(kc, grid, a, st);
     }
   }
   switch (layout) {
     case K1_L256: return launch_k1_reg_f32_L256(kc, grid, a, st);
     case K1_L128: return launch_k1_reg_f32_L128(kc, grid, a, st);
+    case K1_L32M: return launch_k1_reg_f32_L32M(kc, grid, a, st);
+    case K1_L32S: return launch_k1_reg_f32_L32S(kc, grid, a, st);
     default: return launch_k1_reg_f32_L32(kc, grid, a, st);
   }
 }
@@ -104,9 +116,24 @@ Plan make_plan(int dtype, int N, int H, int V, int k, bool dma) {
     p.BH = 128;
     p.BV = 256;
   } else {
-    p.layout = kb::K1_L32;
+    // one row tile: the word tile sets how many CUs take part.  Of 512, 256 and
+    // 128 words, the one with the shortest split (tiles per split x (tile
+    // width + a per-tile cost of about 64 words' worth)) wins; ties keep the
+    // wider tile.
+    static const int kLayouts[3] = {kb::K1_L32, kb::K1_L32M, kb::K1_L32S};
+    long best = -1;
+    for (int i = 0; i < 3; ++i) {
+      const int bv = 512 >> i;
+      const int nt = (V + bv - 1) / bv;
+      const int pp = nt < kTargetCUs ? nt : kTargetCUs;
+      const long cost = (long)((nt + pp - 1) / pp) * (bv + 64);
+      if (best < 0 || cost < best) {
+        best = cost;
+        p.layout = kLayouts[i];
+        p.BV = bv;
+      }
+    }
     p.BH = 32;
-    p.BV = 512;
   }
   p.kc = k <= 4 ? 4 : (k <= 8 ? 8 : (k <= 12 ? 12 : 16));
   p.row_tiles = (N + p.BH - 1) / p.BH;

@@ -39,6 +39,12 @@ SMALL = [
     ([1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15, 16, 17], 64, 5000, 7, "f32"),
     ([40, 3], 64, 60000, 16, "bf16"),          # many splits per row, a sentence of 40 rows
     ([20, 17, 1], 64, 30000, 13, "f32"),       # sentences longer than one merge chunk
+    # few rows: the word tile (512, 256 or 128) follows the vocabulary size
+    ([5], 256, 50000, 5, "bf16"),              # 256-word tiles, DMA pipeline
+    ([3, 2], 128, 20000, 4, "bf16"),           # 128-word tiles, DMA pipeline
+    ([2] * 10, 128, 40000, 12, "bf16"),        # 256-word tiles, k = 12
+    ([4, 4], 64, 40000, 3, "f32"),             # 256-word tiles, register-staged f32
+    ([16, 16], 128, 70000, 16, "bf16"),        # 512-word tiles, k = 16, 32 rows
 ]
 
 
