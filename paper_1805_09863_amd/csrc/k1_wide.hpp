@@ -47,7 +47,7 @@ struct WideGeom {
   static constexpr int HE = BH * BK;  // bf16 elements of h per stage
   static constexpr int OPS = 8;       // DMA instructions per wave per stage
   static constexpr int DMA_SLOT0 = 8; // first MFMA (of each 16) followed by a DMA instruction
-  static constexpr int CAPH = 5;      // candidate slots per row and holder per round
+  static constexpr int CAPH = 8;      // candidate slots per row and holder per round
   static constexpr int DONE = 64;     // "no pending candidates" position
   static constexpr int MS = 16;       // splits that share their running row maxima
 };
@@ -59,13 +59,25 @@ struct alignas(16) WideEpi {
   uint32_t cnt[WideGeom::BH];     // candidates each holder appended to the row this round (one byte each)
   int flag[4];                    // "a lane could not append" of this and the next round
   union {
-    struct {
-      float x[WideGeom::BH][4][WideGeom::CAPH];    // scores appended this round, per row and holder
-      uint8_t p[WideGeom::BH][4][WideGeom::CAPH];  // their positions (0..63) among the holder's scores
-    } c;
+    // positions (0..63), among the holder's scores, of the scores appended this
+    // round per row and holder; the scores themselves go to the idle ring buffer
+    uint8_t p[WideGeom::BH][4][WideGeom::CAPH];
     float red[WideGeom::BH][16];  // seeds, then the per-holder statistics
   } u;
 };
+
+// Candidate scores of a round live in the ring buffer of a tile's last stage
+// (nk is a multiple of 4, so that is always buffer 3): its reads end at the
+// barrier in the middle of that stage, and the next DMA into it is issued in
+// the next tile's first stage, after the epilogue's last barrier.  Slot c of
+// (row r, holder h) is float (4 r + h) * CAPH + (c ^ ((r >> 1) & 7)): the XOR
+// spreads a wave's appends (32 rows x 2 holders, any slot) over 32 banks.
+__device__ __forceinline__ int cand_slot(int r, int h, int c) {
+  return (r * 4 + h) * WideGeom::CAPH + (c ^ ((r >> 1) & 7));
+}
+static_assert(WideGeom::CAPH == 8, "the slot swizzle permutes 8 slots");
+static_assert(WideGeom::BH * 4 * WideGeom::CAPH * 4 <= (WideGeom::WE + WideGeom::HE) * 2,
+              "a round's candidate scores fit in one ring buffer");
 
 // Global->LDS DMA with a wave-uniform base (SGPR pair) and a per-lane 32-bit
 // byte offset: lane i copies 16 bytes from base + voff + OFF to LDS byte
@@ -504,7 +516,8 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
           int newres = G::DONE, c = 0;
           // the lane's slots of the row (LDS byte addresses, opaque so that the
           // per-slot addresses are formed at the store, not kept in registers)
-          uint32_t sx = lds_addr(&ep.u.c.x[rl][holder][0]), sp = lds_addr(&ep.u.c.p[rl][holder][0]);
+          uint32_t sx = lds_addr(S3) + 4u * (uint32_t)((rl * 4 + holder) * G::CAPH), sp = lds_addr(&ep.u.p[rl][holder][0]);
+          const int swz = (rl >> 1) & 7;
           asm volatile("" : "+v"(sx), "+v"(sp));
 #pragma unroll
           for (int vb = 0; vb < 4; ++vb) {
@@ -523,7 +536,7 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
                   if (pred && room) {
                     int pv = pos;  // materialized here, not hoisted (64 constants would pin VGPRs)
                     asm volatile("" : "+v"(pv));
-                    *(KB_LDS float*)(uintptr_t)(sx + 4 * c) = x;
+                    *(KB_LDS float*)(uintptr_t)(sx + 4 * (c ^ swz)) = x;
                     *(KB_LDS uint8_t*)(uintptr_t)(sp + c) = (uint8_t)pv;
                   }
                   c += (pred && room) ? 1 : 0;
@@ -550,11 +563,12 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
             // word of position p of holder hd: holder = 2 wv + half
             const int wb = v0 + (hd >> 1) * 128 + (hd & 1) * 4;
             for (int i = 0; i < c; ++i) {
-              const int p = ep.u.c.p[tid][hd][i];
+              const int p = ep.u.p[tid][hd][i];
+              const float cx = *(KB_LDS const float*)(uintptr_t)(lds_addr(S3) + 4u * (uint32_t)cand_slot(tid, hd, i));
               const int word = wb + (p >> 4) * 32 + ((p >> 2) & 3) * 8 + (p & 3);
-              uint64_t key = cand_key(ep.u.c.x[tid][hd][i], word);
+              uint64_t key = cand_key(cx, word);
               if (key > lkey[KC - 1]) {
-                rowbest = fmaxf(rowbest, ep.u.c.x[tid][hd][i]);
+                rowbest = fmaxf(rowbest, cx);
                 // insertion with independent compares: the keys are descending,
                 // so gt[] is false then true; the key lands at the first true
                 bool gt[KC];
