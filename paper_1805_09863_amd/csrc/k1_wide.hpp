@@ -557,27 +557,29 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
       {
         const uint32_t cw = ep.cnt[tid];
         if (cw != 0u) {
-#pragma unroll
-          for (int hd = 0; hd < 4; ++hd) {
-            const int c = (cw >> (8 * hd)) & 0xFF;
+          // the row's candidates, holder after holder, as one sequence: the
+          // wave loops as long as its longest row, not its longest holder of
+          // each holder in turn
+          const int c0 = cw & 0xFF, c1 = (cw >> 8) & 0xFF, c2 = (cw >> 16) & 0xFF;
+          const int e1 = c0, e2 = c0 + c1, e3 = e2 + c2, tot = e3 + (int)(cw >> 24);
+          for (int i = 0; i < tot; ++i) {
+            const int hd = (i >= e1 ? 1 : 0) + (i >= e2 ? 1 : 0) + (i >= e3 ? 1 : 0);
+            const int j = i - (hd == 0 ? 0 : (hd == 1 ? e1 : (hd == 2 ? e2 : e3)));
+            const int p = ep.u.p[tid][hd][j];
+            const float cx = *(KB_LDS const float*)(uintptr_t)(lds_addr(S3) + 4u * (uint32_t)cand_slot(tid, hd, j));
             // word of position p of holder hd: holder = 2 wv + half
-            const int wb = v0 + (hd >> 1) * 128 + (hd & 1) * 4;
-            for (int i = 0; i < c; ++i) {
-              const int p = ep.u.p[tid][hd][i];
-              const float cx = *(KB_LDS const float*)(uintptr_t)(lds_addr(S3) + 4u * (uint32_t)cand_slot(tid, hd, i));
-              const int word = wb + (p >> 4) * 32 + ((p >> 2) & 3) * 8 + (p & 3);
-              uint64_t key = cand_key(cx, word);
-              if (key > lkey[KC - 1]) {
-                rowbest = fmaxf(rowbest, cx);
-                // insertion with independent compares: the keys are descending,
-                // so gt[] is false then true; the key lands at the first true
-                bool gt[KC];
+            const int word = v0 + (hd >> 1) * 128 + (hd & 1) * 4 + (p >> 4) * 32 + ((p >> 2) & 3) * 8 + (p & 3);
+            uint64_t key = cand_key(cx, word);
+            if (key > lkey[KC - 1]) {
+              rowbest = fmaxf(rowbest, cx);
+              // insertion with independent compares: the keys are descending,
+              // so gt[] is false then true; the key lands at the first true
+              bool gt[KC];
 #pragma unroll
-                for (int j = 0; j < KC; ++j) gt[j] = key > lkey[j];
+              for (int jj = 0; jj < KC; ++jj) gt[jj] = key > lkey[jj];
 #pragma unroll
-                for (int j = KC - 1; j > 0; --j) lkey[j] = gt[j] ? (gt[j - 1] ? lkey[j - 1] : key) : lkey[j];
-                lkey[0] = gt[0] ? key : lkey[0];
-              }
+              for (int jj = KC - 1; jj > 0; --jj) lkey[jj] = gt[jj] ? (gt[jj - 1] ? lkey[jj - 1] : key) : lkey[jj];
+              lkey[0] = gt[0] ? key : lkey[0];
             }
           }
           ep.cnt[tid] = 0u;
