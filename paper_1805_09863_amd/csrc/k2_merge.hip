@@ -143,21 +143,24 @@ __global__ __launch_bounds__(1024) void k2_merge(K2Args a) {
     const int r = cr0 + ri;
     float2 st[NQ];
     if (active) {
-      // lane = 16 * g + j stages entry j of lists p0 + g, p0 + 4 + g, ...
-      // (slots j >= k get empty entries): 32 lists per pass, eight loads in
-      // flight per lane before the first LDS write
-      const int j = lane & 15, g = lane >> 4;
-      for (int p0 = 0; p0 < P; p0 += 32) {
+      // lane = kp * g + j (kp: k rounded up to a power of two) stages entry j
+      // of lists p0 + g, p0 + gpl + g, ... (gpl = 64 / kp lists per load;
+      // slots k .. kp - 1 get empty entries): eight loads in flight per lane
+      // before the first LDS write.  Slots past kp are never read before a
+      // list has given up all k entries, so they stay unwritten.
+      const int lgk = k <= 1 ? 0 : (k <= 2 ? 1 : (k <= 4 ? 2 : (k <= 8 ? 3 : 4)));
+      const int j = lane & ((1 << lgk) - 1), g = lane >> lgk, gpl = 64 >> lgk;
+      for (int p0 = 0; p0 < P; p0 += 8 * gpl) {
         int2 v[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
-          const int p = p0 + 4 * u + g;
+          const int p = p0 + u * gpl + g;
           v[u] = make_int2(kNegInfBits, INT_MAX);
           if (p < P && j < k) v[u] = a.lists[((size_t)p * a.N + r) * k + j];
         }
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
-          const int p = p0 + 4 * u + g;
+          const int p = p0 + u * gpl + g;
           if (p < P) lists_dyn[wbase + p * K2_LS + j] = v[u];
         }
       }
@@ -321,10 +324,12 @@ hipError_t launch_k2_argmax(const int2* lists, int P, int N, int32_t* tok, float
 
 template <int NQ>
 static hipError_t launch_k2_nq(const K2Args& a, hipStream_t st) {
-  // as many waves (rows at once) as the staged lists fit in 144 KB of LDS
-  // (the kernel's static LDS is under 4 KB): 16 up to P = 72, 4 at P = 256
+  // one wave per row of a sentence of average length (longer sentences take
+  // their rows in chunks), as many as the staged lists fit in 144 KB of LDS
+  // (the kernel's static LDS is under 4 KB): at most 16 up to P = 72, 4 at P = 256
   const size_t per_wave = (size_t)a.P * K2_LS * sizeof(int2);
-  const int W = (int)std::min<size_t>(K2_MAXW, (144 * 1024) / per_wave);
+  const int rows_per = (a.N + a.S - 1) / a.S;
+  const int W = (int)std::min<size_t>(std::min(K2_MAXW, std::max(1, rows_per)), (144 * 1024) / per_wave);
   const size_t lds = (size_t)K2_LS * sizeof(int2) + (size_t)W * per_wave;
   if (lds > 48 * 1024) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k2_merge<NQ>),
