@@ -45,6 +45,7 @@ SMALL = [
     ([2] * 10, 128, 40000, 12, "bf16"),        # 256-word tiles, k = 12
     ([4, 4], 64, 40000, 3, "f32"),             # 256-word tiles, register-staged f32
     ([16, 16], 128, 70000, 16, "bf16"),        # 512-word tiles, k = 16, 32 rows
+    ([2, 3, 1], 128, 20000, 2, "bf16"),        # k = 2: merge lanes staged in pairs
 ]
 
 
