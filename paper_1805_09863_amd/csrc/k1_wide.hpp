@@ -58,6 +58,8 @@ struct alignas(16) WideEpi {
   float thr[WideGeom::BH];        // row's local threshold: its k-th best so far, or the seed
   uint32_t cnt[WideGeom::BH];     // candidates each holder appended to the row this round (one byte each)
   int flag[4];                    // "a lane could not append" of this and the next round
+  float trash_x[4 * 64];          // per lane: where a score that takes no slot is written
+  uint8_t trash_p[4 * 64];
   union {
     // positions (0..63), among the holder's scores, of the scores appended this
     // round per row and holder; the scores themselves go to the idle ring buffer
@@ -518,7 +520,8 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
           // per-slot addresses are formed at the store, not kept in registers)
           uint32_t sx = lds_addr(S3) + 4u * (uint32_t)((rl * 4 + holder) * G::CAPH), sp = lds_addr(&ep.u.p[rl][holder][0]);
           const int swz = (rl >> 1) & 7;
-          asm volatile("" : "+v"(sx), "+v"(sp));
+          uint32_t tx = lds_addr(&ep.trash_x[tid]), tp = lds_addr(&ep.trash_p[tid]);
+          asm volatile("" : "+v"(sx), "+v"(sp), "+v"(tx), "+v"(tp));
 #pragma unroll
           for (int vb = 0; vb < 4; ++vb) {
             opaque(acc[vb][hb]);  // only this block's 16 scores in VGPRs at a time
@@ -533,13 +536,14 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
                   const bool pred = x >= t && pos >= rs;
                   const bool room = c < G::CAPH;
                   newres = (pred && !room) ? min(newres, pos) : newres;
-                  if (pred && room) {
-                    int pv = pos;  // materialized here, not hoisted (64 constants would pin VGPRs)
-                    asm volatile("" : "+v"(pv));
-                    *(KB_LDS float*)(uintptr_t)(sx + 4 * (c ^ swz)) = x;
-                    *(KB_LDS uint8_t*)(uintptr_t)(sp + c) = (uint8_t)pv;
-                  }
-                  c += (pred && room) ? 1 : 0;
+                  const bool ok = pred && room;
+                  int pv = pos;  // materialized here, not hoisted (64 constants would pin VGPRs)
+                  asm volatile("" : "+v"(pv));
+                  // every lane stores: a score that takes no slot goes to the lane's own
+                  // discard slot, so the appends need no branch
+                  *(KB_LDS float*)(uintptr_t)(ok ? sx + 4 * (c ^ swz) : tx) = x;
+                  *(KB_LDS uint8_t*)(uintptr_t)(ok ? sp + c : tp) = (uint8_t)pv;
+                  c += ok ? 1 : 0;
                 }
               }
             }
