@@ -498,7 +498,8 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
     // row's threshold to its own CAPH slots of the row; past CAPH it notes the
     // first position it could not append and resumes there in the next round,
     // against the raised threshold.  Quads are skipped unless some lane of the
-    // wave needs them, and appends use masked stores, not branches.
+    // wave needs them; inside a quad every lane stores each score, to its next
+    // slot or to its own discard slot, so the appends take no branch.
     int resume[4];
 #pragma unroll
     for (int hb = 0; hb < 4; ++hb) {

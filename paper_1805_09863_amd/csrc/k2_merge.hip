@@ -1,9 +1,10 @@
 // K2: merge the vocabulary splits of every row, then the rows of every sentence.
 //
-// One workgroup per sentence, W waves (W <= 16, as many as the staged lists
-// fit in LDS); the sentence's rows are taken W at a time, one per wave:
-//   * the row's P split lists are staged in LDS, all loads in flight, and its
-//     P split statistics held in registers;
+// One workgroup per sentence, W waves (one per row of an average sentence,
+// W <= 16, and no more than the staged lists fit in LDS); the sentence's rows
+// are taken W at a time, one per wave:
+//   * the row's P split lists are staged in LDS, eight loads in flight per
+//     lane, and its P split statistics held in registers;
 //   * LSE = M + ln(sum_p s_p * exp(m_p - M)) over the P split partials -- the
 //     rescaling identity of Algorithm 4 applied between shards, the reduction
 //     step of Algorithm 6 extended from (max, best) to softmax statistics;
