@@ -575,10 +575,12 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
             // word of position p of holder hd: holder = 2 wv + half
             const int word = v0 + (hd >> 1) * 128 + (hd & 1) * 4 + (p >> 4) * 32 + ((p >> 2) & 3) * 8 + (p & 3);
             uint64_t key = cand_key(cx, word);
-            if (key > lkey[KC - 1]) {
-              rowbest = fmaxf(rowbest, cx);
-              // insertion with independent compares: the keys are descending,
-              // so gt[] is false then true; the key lands at the first true
+            {
+              rowbest = key > lkey[KC - 1] ? fmaxf(rowbest, cx) : rowbest;
+              // insertion with independent compares, without a branch: the keys
+              // are descending, so gt[] is false then true and the key lands at
+              // the first true; a key below the k-th leaves gt[] all false and
+              // the list unchanged
               bool gt[KC];
 #pragma unroll
               for (int jj = 0; jj < KC; ++jj) gt[jj] = key > lkey[jj];
