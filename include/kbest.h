@@ -272,6 +272,59 @@ int kb_beam_backtrace(int S0, int k, int T, float alpha, const int32_t* fin_coun
 int kb_gather_rows(int n_max, const int32_t* n_dev, const int32_t* idx,
                    const void* src, void* dst, size_t row_bytes, void* stream);
 
+/*
+ * Vocabulary shards -- one device's part of the step when the vocabulary is
+ * split across devices (Section 2.2, Algorithm 6: every shard finds the best
+ * of its own range, then one reduction over the shards' results).  Device g
+ * holds W_g = W[:, base_g : base_g + V_g] (contiguous, H x V_g) and b_g, runs
+ * kb_shard_partials into its slice of the combined partial arrays, the
+ * arrays are exchanged (an all-gather of N * (8 + 8k) bytes per split), and
+ * kb_merge_partials over all splits gives exactly kb_kbest_step's result.
+ *
+ * Partial layout, split-major with rows N apart (one split = one vocabulary
+ * range of one shard):
+ *   stats  P x N x 2 float32: per split and row the running max m and
+ *          sum of exp(x - m) over the split's words (Algorithm 4's pair);
+ *   lists  P x N x k x 2 int32: per split and row its k best (score bits,
+ *          word) sorted by (score desc, word asc), words already global;
+ *          entries past a split's words hold a score below every real one.
+ *
+ * kb_shard_splits -- *splits = the number of splits kb_shard_partials writes
+ * for these operands (it depends on the shape and on the pointers' 16-byte
+ * alignment, as the projection's plan does); 0 when N == 0.
+ * kb_shard_workspace_bytes -- workspace kb_shard_partials needs (0 when N == 0).
+ *
+ * kb_shard_partials -- the fused projection over one shard:
+ *   dtype, N, H, k   as kb_kbest_step (k <= V_shard);
+ *   V_shard          the shard's words; word_base its first word's global
+ *                    index (0 <= word_base, word_base + V_shard <= INT_MAX);
+ *   h                N x H; W_shard H x V_shard row-major; b_shard V_shard;
+ *   stats, lists     where this shard's *splits splits go (8-byte aligned),
+ *                    normally the shard's slice of the combined arrays.
+ *   Asynchronous on `stream`; the workspace is scratch (same rules as
+ *   kb_kbest_step).
+ *
+ * kb_merge_partials -- the reduction over the shards and the beam merge:
+ *   N, V, k, S       rows, the whole vocabulary's size, outputs per sentence,
+ *                    sentences (k <= min(KB_MAX_K, V));
+ *   P                total splits of all shards, 1 <= P <= 256;
+ *   stats, lists     the combined partials (layout above);
+ *   prev_score, sent_offsets, out_* as kb_kbest_step (out_row_lse nullable).
+ *   Token, parent and score follow kb_kbest_step's order and tie rule.
+ */
+int kb_shard_splits(int dtype, int N, int H, int V_shard, int k, const void* h,
+                    const void* W_shard, const float* b_shard, int* splits);
+size_t kb_shard_workspace_bytes(int dtype, int N, int H, int V_shard, int k);
+int kb_shard_partials(int dtype, int N, int H, int V_shard, int word_base, int k,
+                      const void* h, const void* W_shard, const float* b_shard,
+                      float* stats, int32_t* lists,
+                      void* workspace, size_t workspace_bytes, void* stream);
+int kb_merge_partials(int N, int V, int k, int S, int P, const float* stats,
+                      const int32_t* lists, const float* prev_score,
+                      const int32_t* sent_offsets, int32_t* out_token,
+                      int32_t* out_parent, float* out_score, float* out_row_lse,
+                      void* stream);
+
 #ifdef __cplusplus
 } /* extern "C" */
 #endif

@@ -43,6 +43,10 @@ SIGNATURES = {
     "kb_beam_backtrace": (_I, [_I, _I, _I, ctypes.c_float, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "kb_compact_batch": (_I, [_I, _I, _P, _P, _P, _P, _P, _P, _P]),
     "kb_gather_rows": (_I, [_I, _P, _P, _P, _P, _SZ, _P]),
+    "kb_shard_splits": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _P]),
+    "kb_shard_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I]),
+    "kb_shard_partials": (_I, [_I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "kb_merge_partials": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     # decoder stand-in of the synthetic decode loop (include/kbest_standin.h)
     "kb_standin_alive": (_I, [_I, _I, _I, _P, _P, _P, _P]),
     "kb_standin_next_h": (_I, [_I, _P, _I, _I, _I, _P, _P, _P, _P, _SZ, _P]),
@@ -272,6 +276,64 @@ def gather_rows(src: torch.Tensor, idx: torch.Tensor, *, n_dev: Optional[torch.T
 
 
 # ---------------------------------------------------------------- decoder stand-in
+def shard_splits(h: torch.Tensor, W_shard: torch.Tensor, b_shard: torch.Tensor, k: int) -> int:
+    """Number of vocabulary splits shard_partials writes for these operands."""
+    N, H = h.shape
+    out = ctypes.c_int(0)
+    _check(lib().kb_shard_splits(_dtype_code(h), N, H, W_shard.shape[1], k, _ptr(h), _ptr(W_shard), _ptr(b_shard),
+                                 ctypes.byref(out)))
+    return int(out.value)
+
+
+def shard_partials(h: torch.Tensor, W_shard: torch.Tensor, b_shard: torch.Tensor, k: int, word_base: int,
+                   stats: torch.Tensor, lists: torch.Tensor, *, ws: Optional[torch.Tensor] = None, stream=None):
+    """One vocabulary shard's fused projection (see include/kbest.h): its splits'
+    statistics into ``stats`` (splits x N x 2 float32) and k-best lists into
+    ``lists`` (splits x N x k x 2 int32, global words), normally slices of the
+    combined arrays that merge_partials reduces."""
+    _need(h, "h", dim=2)
+    _need(W_shard, "W_shard", dtype=h.dtype, dim=2)
+    _need(b_shard, "b_shard", dtype=torch.float32, dim=1)
+    _need(stats, "stats", dtype=torch.float32)
+    _need(lists, "lists", dtype=torch.int32)
+    N, H = h.shape
+    if W_shard.shape[0] != H or b_shard.shape[0] != W_shard.shape[1]:
+        raise ValueError("shape mismatch among h, W_shard, b_shard")
+    V_shard = W_shard.shape[1]
+    P = shard_splits(h, W_shard, b_shard, k)
+    if stats.numel() < P * N * 2 or lists.numel() < P * N * k * 2:
+        raise ValueError(f"stats / lists too small for {P} splits")
+    dt = _dtype_code(h)
+    if ws is None:
+        ws = workspace(lib().kb_shard_workspace_bytes(dt, N, H, V_shard, k), h.device)
+    _check(lib().kb_shard_partials(dt, N, H, V_shard, word_base, k, _ptr(h), _ptr(W_shard), _ptr(b_shard),
+                                   _ptr(stats), _ptr(lists), _ptr(ws), ws.numel() * ws.element_size(),
+                                   _stream(stream)))
+    return P
+
+
+def merge_partials(stats: torch.Tensor, lists: torch.Tensor, P: int, V: int, k: int, prev_score: torch.Tensor,
+                   sent_offsets: torch.Tensor, *, out: Optional[tuple] = None,
+                   row_lse: Optional[torch.Tensor] = None, stream=None):
+    """Reduce the combined partials of all shards (P splits in total) and merge the
+    beam: returns (token, parent, score), each S x k, as kbest_step does."""
+    _need(stats, "stats", dtype=torch.float32)
+    _need(lists, "lists", dtype=torch.int32)
+    _need(prev_score, "prev_score", dtype=torch.float32, dim=1)
+    _need(sent_offsets, "sent_offsets", dtype=torch.int32, dim=1)
+    N = prev_score.shape[0]
+    S = sent_offsets.shape[0] - 1
+    if stats.numel() < P * N * 2 or lists.numel() < P * N * k * 2:
+        raise ValueError(f"stats / lists too small for {P} splits")
+    if out is None:
+        out = tuple(torch.empty((S, k), dtype=t, device=prev_score.device)
+                    for t in (torch.int32, torch.int32, torch.float32))
+    tok, par, sc = out
+    _check(lib().kb_merge_partials(N, V, k, S, P, _ptr(stats), _ptr(lists), _ptr(prev_score), _ptr(sent_offsets),
+                                   _ptr(tok), _ptr(par), _ptr(sc), _ptr(row_lse), _stream(stream)))
+    return tok, par, sc
+
+
 def standin_alive(sid: torch.Tensor, lengths: torch.Tensor, S: int, k: int, t: int, *, out: torch.Tensor,
                   stream=None) -> torch.Tensor:
     """out[s*k + r] = (t < lengths[sid[s]] - 1) for s < S (include/kbest_standin.h)."""

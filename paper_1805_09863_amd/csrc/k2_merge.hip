@@ -341,6 +341,23 @@ static hipError_t launch_k2_nq(const K2Args& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// A vocabulary shard's partial lists hold shard-local words; this moves them
+// to the shard's place in the whole vocabulary.  Empty entries (word -1 or
+// INT_MAX, score below every real one) keep their word.
+__global__ __launch_bounds__(256) void add_word_base(int2* __restrict__ lists, size_t n, int base, int v_shard) {
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) {
+    const int w = lists[i].y;
+    if ((unsigned)w < (unsigned)v_shard) lists[i].y = w + base;
+  }
+}
+
+hipError_t launch_add_word_base(int2* lists, size_t n, int base, int v_shard, hipStream_t st) {
+  if (n == 0 || base == 0) return hipSuccess;
+  const int blocks = (int)std::min<size_t>((n + 255) / 256, 2048);
+  add_word_base<<<dim3(blocks), dim3(256), 0, st>>>(lists, n, base, v_shard);
+  return hipGetLastError();
+}
+
 hipError_t launch_k2(const K2Args& a, hipStream_t st) {
   if (a.P < 1 || a.P > 64 * K2_LPL || a.k < 1 || a.k > K2_LS) return hipErrorInvalidValue;
   if (a.S <= 0) return hipSuccess;

@@ -113,6 +113,7 @@ struct K2Args {
 };
 
 hipError_t launch_k2(const K2Args& a, hipStream_t st);
+hipError_t launch_add_word_base(int2* lists, size_t n, int base, int v_shard, hipStream_t st);
 hipError_t launch_k2_argmax(const int2* lists, int P, int N, int32_t* tok, float* val, hipStream_t st);
 
 // ---------------------------------------------------------------- K3 / gather

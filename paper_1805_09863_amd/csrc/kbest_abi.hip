@@ -175,17 +175,27 @@ int validate_step(int dtype, int N, int H, int V, int k, int S) {
   return KB_OK;
 }
 
+// Whether the operands allow 16-byte vector loads, and the plan they select.
+bool vec_operands(int dtype, int H, int V, const void* h, const void* W) {
+  const int vec = dtype == KB_BF16 ? 8 : 4;
+  return (H % vec == 0) && (V % vec == 0) && aligned(h, 16) && aligned(W, 16);
+}
+Plan plan_for(int dtype, int N, int H, int V, int k, const void* h, const void* W, const float* b) {
+  const bool dma = dma_shape(dtype, H, V) && vec_operands(dtype, H, V, h, W) && aligned(b, 16);
+  return make_plan(dtype, N, H, V, k, dma);
+}
+
 // Alignment checks, plan, threshold reset and the projection kernel (K1)
-// shared by the k-best step and the greedy argmax.  On KB_OK, a1 and p
-// describe the launched projection; its partials are in the workspace.
+// shared by the k-best step, the greedy argmax and the vocabulary shards.  On
+// KB_OK, a1 and p describe the launched projection; its partials are in the
+// workspace, or in stats_out / lists_out when given (split rows N apart).
 int launch_projection(int dtype, int N, int H, int V, int k, const void* h, const void* W, const float* b,
                       void* ws, size_t ws_bytes, hipStream_t hs, bool no_stats, void* ev0, void* ev1,
-                      kb::K1Args& a1, Plan& p) {
+                      kb::K1Args& a1, Plan& p, float2* stats_out = nullptr, int2* lists_out = nullptr) {
   const size_t esz = dtype == KB_BF16 ? 2 : 4;
   if (!aligned(h, esz) || !aligned(W, esz) || !aligned(b, 4))
     return fail(KB_ERR_INVALID_ARG, "h, W or b misaligned for its element type");
-  const int vec = dtype == KB_BF16 ? 8 : 4;
-  const bool vec_ok = (H % vec == 0) && (V % vec == 0) && aligned(h, 16) && aligned(W, 16);
+  const bool vec_ok = vec_operands(dtype, H, V, h, W);
   const bool dma = dma_shape(dtype, H, V) && vec_ok && aligned(b, 16);
   p = make_plan(dtype, N, H, V, k, dma);
   const size_t need = workspace_bytes(dtype, N, H, V, k);
@@ -205,8 +215,8 @@ int launch_projection(int dtype, int N, int H, int V, int k, const void* h, cons
   a1.tps = p.tps;
   a1.n_vtiles = p.n_vtiles;
   a1.vec_ok = vec_ok;
-  a1.stats = reinterpret_cast<float2*>((char*)ws + p.stats_off);
-  a1.lists = reinterpret_cast<int2*>((char*)ws + p.lists_off);
+  a1.stats = stats_out ? stats_out : reinterpret_cast<float2*>((char*)ws + p.stats_off);
+  a1.lists = lists_out ? lists_out : reinterpret_cast<int2*>((char*)ws + p.lists_off);
   a1.gthr = reinterpret_cast<uint32_t*>((char*)ws + p.gthr_off);
   a1.gmax = reinterpret_cast<uint32_t*>((char*)ws + p.gmax_off);
   a1.row_tiles = p.row_tiles;
@@ -503,6 +513,80 @@ int kb_gather_rows(int n_max, const int32_t* n_dev, const int32_t* idx, const vo
   if (!aligned(src, 4) || !aligned(dst, 4)) return fail(KB_ERR_INVALID_ARG, "src and dst must be 4-byte aligned");
   hipError_t e = kb::launch_gather(n_max, n_dev, idx, src, dst, row_bytes, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(KB_ERR_HIP, "gather kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+// ---- vocabulary shards (Algorithm 6 across devices): one GPU's part
+int kb_shard_splits(int dtype, int N, int H, int V_shard, int k, const void* h, const void* W_shard,
+                    const float* b_shard, int* splits) {
+  if (!splits) return fail(KB_ERR_INVALID_ARG, "splits is null");
+  int st = validate_step(dtype, N, H, V_shard, k, N > 0 ? 1 : 0);
+  if (st != KB_OK) return st;
+  if (N == 0) {
+    *splits = 0;
+    return ok();
+  }
+  if (!h || !W_shard || !b_shard) return fail(KB_ERR_INVALID_ARG, "null h, W_shard or b_shard");
+  *splits = plan_for(dtype, N, H, V_shard, k, h, W_shard, b_shard).P;
+  return ok();
+}
+
+size_t kb_shard_workspace_bytes(int dtype, int N, int H, int V_shard, int k) {
+  if (N <= 0 || H < 1 || V_shard < 1 || k < 1 || k > KB_MAX_K) return 0;
+  return workspace_bytes(dtype, N, H, V_shard, k);
+}
+
+int kb_shard_partials(int dtype, int N, int H, int V_shard, int word_base, int k, const void* h,
+                      const void* W_shard, const float* b_shard, float* stats, int32_t* lists, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+  int st = validate_step(dtype, N, H, V_shard, k, N > 0 ? 1 : 0);
+  if (st != KB_OK) return st;
+  if (N == 0) return ok();
+  if (!h || !W_shard || !b_shard || !stats || !lists) return fail(KB_ERR_INVALID_ARG, "null input or output pointer");
+  if (word_base < 0 || (long long)word_base + V_shard > INT_MAX)
+    return fail(KB_ERR_INVALID_ARG, "word_base = %d outside [0, INT_MAX - V_shard]", word_base);
+  if (!aligned(stats, 8) || !aligned(lists, 8)) return fail(KB_ERR_INVALID_ARG, "stats and lists must be 8-byte aligned");
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  kb::K1Args a1;
+  Plan p;
+  st = launch_projection(dtype, N, H, V_shard, k, h, W_shard, b_shard, workspace, workspace_bytes, hs, false, nullptr,
+                         nullptr, a1, p, reinterpret_cast<float2*>(stats), reinterpret_cast<int2*>(lists));
+  if (st != KB_OK) return st;
+  hipError_t e = kb::launch_add_word_base(reinterpret_cast<int2*>(lists), (size_t)p.P * N * k, word_base, V_shard, hs);
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "word offset kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int kb_merge_partials(int N, int V, int k, int S, int P, const float* stats, const int32_t* lists,
+                      const float* prev_score, const int32_t* sent_offsets, int32_t* out_token, int32_t* out_parent,
+                      float* out_score, float* out_row_lse, void* stream) {
+  if (N < 0 || S < 0) return fail(KB_ERR_INVALID_ARG, "negative N (%d) or S (%d)", N, S);
+  if ((N == 0) != (S == 0)) return fail(KB_ERR_INVALID_ARG, "N = %d and S = %d: both or neither must be 0", N, S);
+  if (N < S) return fail(KB_ERR_INVALID_ARG, "N = %d < S = %d: every sentence needs a row", N, S);
+  if (V < 1) return fail(KB_ERR_INVALID_ARG, "V = %d must be >= 1", V);
+  if (k < 1 || k > KB_MAX_K || k > V) return fail(KB_ERR_INVALID_ARG, "k = %d outside [1, min(%d, V = %d)]", k, KB_MAX_K, V);
+  if (P < 1 || P > 256) return fail(KB_ERR_UNSUPPORTED, "P = %d splits outside [1, 256]", P);
+  if ((long long)N * k * P > INT_MAX || (long long)N * V > (1LL << 46)) return fail(KB_ERR_UNSUPPORTED, "shape too large");
+  if (N == 0) return ok();
+  if (!stats || !lists || !prev_score || !sent_offsets || !out_token || !out_parent || !out_score)
+    return fail(KB_ERR_INVALID_ARG, "null input or output pointer");
+  if (!aligned(stats, 8) || !aligned(lists, 8)) return fail(KB_ERR_INVALID_ARG, "stats and lists must be 8-byte aligned");
+  kb::K2Args a2{};
+  a2.stats = reinterpret_cast<const float2*>(stats);
+  a2.lists = reinterpret_cast<const int2*>(lists);
+  a2.P = P;
+  a2.N = N;
+  a2.V = V;
+  a2.k = k;
+  a2.S = S;
+  a2.prev = prev_score;
+  a2.off = sent_offsets;
+  a2.tok = out_token;
+  a2.par = out_parent;
+  a2.score = out_score;
+  a2.row_lse = out_row_lse;
+  hipError_t e = kb::launch_k2(a2, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "merge kernel launch: %s", hipGetErrorString(e));
   return ok();
 }
 

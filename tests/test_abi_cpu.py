@@ -160,3 +160,40 @@ def test_beam_argument_checks():
     assert L.kb_beam_backtrace(0, 4, 10, 1.0, *fin, FAKE, FAKE, *out, None) == KB_OK
     assert L.kb_beam_backtrace(5, 4, 0, 1.0, *fin, FAKE, FAKE, *out, None) == KB_ERR_INVALID_ARG
     assert L.kb_beam_backtrace(5, 4, 10, 1.0, *fin, None, FAKE, *out, None) == KB_ERR_INVALID_ARG
+
+
+def test_shard_argument_checks():
+    L = binding.lib()
+    n = ctypes.c_int(-1)
+    # splits follow the projection's plan: 3072 rows x 11,256 words (V=90k over 8 devices, cut on
+    # multiples of 8), 16-byte aligned bf16 operands -> 12 row tiles x 15 splits of 3 word tiles
+    assert L.kb_shard_splits(1, 3072, 1024, 11256, 12, FAKE, FAKE, FAKE, ctypes.byref(n)) == KB_OK
+    assert n.value == 15
+    # 11,250 words (V % 8 != 0) take the register-staged kernel's 128-word tiles: 18 splits of 5
+    assert L.kb_shard_splits(1, 3072, 1024, 11250, 12, FAKE, FAKE, FAKE, ctypes.byref(n)) == KB_OK
+    assert n.value == 18
+    assert L.kb_shard_splits(1, 0, 1024, 11250, 12, None, None, None, ctypes.byref(n)) == KB_OK and n.value == 0
+    assert L.kb_shard_splits(1, 3072, 1024, 11250, 12, FAKE, FAKE, FAKE, None) == KB_ERR_INVALID_ARG
+    assert L.kb_shard_splits(1, 64, 1024, 8, 12, FAKE, FAKE, FAKE, ctypes.byref(n)) == KB_ERR_INVALID_ARG   # k > V
+    assert L.kb_shard_workspace_bytes(1, 3072, 1024, 11250, 12) > 0
+    assert L.kb_shard_workspace_bytes(1, 0, 1024, 11250, 12) == 0
+    # kb_shard_partials(dtype, N, H, V_shard, word_base, k, h, W, b, stats, lists, ws, ws_bytes, stream)
+    sp = L.kb_shard_partials
+    assert sp(1, 0, 128, 1000, 0, 5, None, None, None, None, None, None, 0, None) == KB_OK   # empty batch
+    assert sp(1, 10, 128, 1000, -1, 5, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == KB_ERR_INVALID_ARG
+    assert sp(1, 10, 128, 1000, (1 << 31) - 100, 5, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30,
+              None) == KB_ERR_INVALID_ARG                                                        # base + V overflows
+    assert sp(1, 10, 128, 1000, 0, 5, FAKE, FAKE, FAKE, None, FAKE, FAKE, 1 << 30, None) == KB_ERR_INVALID_ARG
+    assert sp(1, 10, 128, 1000, 0, 5, FAKE, FAKE, FAKE, ctypes.c_void_p(0x1004), FAKE, FAKE, 1 << 30,
+              None) == KB_ERR_INVALID_ARG                                                        # stats alignment
+    assert sp(1, 10, 128, 1000, 0, 5, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 16, None) == KB_ERR_WORKSPACE
+    # kb_merge_partials(N, V, k, S, P, stats, lists, prev, off, tok, par, score, lse, stream)
+    mp = L.kb_merge_partials
+    out = [FAKE] * 7
+    assert mp(0, 1000, 5, 0, 4, *out, None, None) == KB_OK                                       # empty batch
+    assert mp(10, 1000, 5, 2, 0, *out, None, None) == KB_ERR_UNSUPPORTED                         # P < 1
+    assert mp(10, 1000, 5, 2, 257, *out, None, None) == KB_ERR_UNSUPPORTED                       # P > 256
+    assert mp(10, 1000, 17, 2, 4, *out, None, None) == KB_ERR_INVALID_ARG                        # k > 16
+    assert mp(10, 4, 5, 2, 4, *out, None, None) == KB_ERR_INVALID_ARG                            # k > V
+    assert mp(2, 1000, 5, 3, 4, *out, None, None) == KB_ERR_INVALID_ARG                          # N < S
+    assert mp(10, 1000, 5, 2, 4, None, *out[1:], None, None) == KB_ERR_INVALID_ARG
