@@ -274,6 +274,54 @@ def ablation_bench(torch, np, kb, reps: int = 10):
             "reps": reps, "rows": rows, "greedy_beam1": greedy, "precision": prec}
 
 
+def shard_bench(torch, np, kb, reps: int = 20):
+    """One device's part of a vocabulary-split step (Algorithm 6 across devices):
+    the V=90k workload cut into 8 shards on multiples of 8 words; each shard's
+    fused projection and the merge of all shards' partials, timed with events
+    on the stream, next to the whole step on one device.  The all-gather of the
+    partials between devices is not built; its size is reported."""
+    from synth import workloads as wl
+    inp = wl.make_workload(wl.V90K)
+    h, W, b, prev, off = to_dev(inp, torch, np)
+    N, k, V = inp.N, inp.k, inp.V
+    cuts = [11256 * i for i in range(8)] + [V]
+    shards = [(a, W[:, a:z].contiguous(), b[a:z].contiguous()) for a, z in zip(cuts, cuts[1:])]
+    Ps = [kb.shard_splits(h, Wg, bg, k) for _, Wg, bg in shards]
+    P = sum(Ps)
+    stats = torch.empty((P, N, 2), dtype=torch.float32, device="cuda")
+    lists = torch.empty((P, N, k, 2), dtype=torch.int32, device="cuda")
+    wss = [kb.workspace(kb.binding.lib().kb_shard_workspace_bytes(kb.KB_BF16, N, inp.H, Wg.shape[1], k))
+           for _, Wg, _ in shards]
+    offs = np.concatenate([[0], np.cumsum(Ps)]).tolist()
+    out = tuple(torch.empty((inp.S, k), dtype=t, device="cuda") for t in (torch.int32, torch.int32, torch.float32))
+    ws_full = kb.workspace(kb.kbest_workspace_bytes(kb.KB_BF16, N, inp.H, V, k, inp.S))
+
+    def timed(fn):
+        for _ in range(5):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    shard_ms = []
+    for i, (a, Wg, bg) in enumerate(shards):
+        sl = slice(offs[i], offs[i + 1])
+        shard_ms.append(timed(lambda: kb.shard_partials(h, Wg, bg, k, a, stats[sl], lists[sl], ws=wss[i])))
+    merge_ms = timed(lambda: kb.merge_partials(stats, lists, P, V, k, prev, off, out=out))
+    whole_ms = timed(lambda: kb.kbest_step(h, W, b, prev, off, k, out=out, ws=ws_full))
+    flops = 2.0 * N * inp.H * 11256
+    return {"workload": f"{inp.name} over 8 vocabulary shards (7 x 11256 + {V - 7 * 11256} words)",
+            "splits_per_shard": Ps, "shard_ms": shard_ms, "shard_tflops": flops / (max(shard_ms) * 1e-3) / 1e12,
+            "merge_ms": merge_ms, "one_device_share_ms": max(shard_ms) + merge_ms, "whole_step_one_device_ms": whole_ms,
+            "exchange_bytes_per_device": Ps[0] * N * (8 + 8 * k),
+            "note": "the all-gather of the partials between devices is not built (one GPU); its size is given"}
+
+
 def sweep_bench(torch, np, kb):
     """Step time against the number of rows, the per-step time of a 1280-sentence
     decode (compacted and naive), and decode throughput against the number of
@@ -400,6 +448,9 @@ def main():
     ap.add_argument("--sweep", action="store_true",
                     help="only run the row-count and batch-size sweeps and the per-step curves of a "
                          "1280-sentence decode, print them as the JSON line and exit")
+    ap.add_argument("--shards", action="store_true",
+                    help="only time one device's part of a step split over 8 vocabulary shards (each shard's "
+                         "projection and the merge of all partials) at V=90k, print it as the JSON line and exit")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB three times (to scale HBM "
                          "byte counters against a kernel of known traffic), then exit")
@@ -429,6 +480,12 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "launches": 3}))
+        return
+    if args.shards:
+        kb.lib()
+        res = {"metric": "vocabulary-split step, one device's part", "unit": "ms", "data": "synthetic (seeded)",
+               "n_gpus": 1, "shards": shard_bench(torch, np, kb)}
+        print(json.dumps(res), flush=True)
         return
     if args.ablation or args.sweep:
         kb.lib()
