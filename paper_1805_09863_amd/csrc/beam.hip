@@ -13,7 +13,7 @@
 // beam_backtrace, one thread per sentence: the finished hypothesis with the
 // best length-normalised score (score / length^alpha; ties: the earlier one)
 // and its tokens, read back through the history.
-#include "kb_common.hpp"
+#include "kb_launch.hpp"
 
 namespace kb {
 

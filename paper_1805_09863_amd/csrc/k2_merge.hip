@@ -20,7 +20,7 @@
 //     kept.  Because the score adds a per-row constant to x, a sentence's k
 //     best lie in the union of its rows' k best, so nothing outside these
 //     candidates can be selected.
-#include "kb_common.hpp"
+#include "kb_launch.hpp"
 
 namespace kb {
 

@@ -6,7 +6,7 @@
 // and each survivor writes its index at its rank.  A second pass does the same
 // over sentences with a packed (surviving sentence, surviving entries) count
 // to build the new offsets.  Integer work only: results are exact.
-#include "kb_common.hpp"
+#include "kb_launch.hpp"
 
 namespace kb {
 

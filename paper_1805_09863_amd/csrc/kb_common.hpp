@@ -99,54 +99,4 @@ enum K1Layout { K1_L256 = 0, K1_L128 = 1, K1_L32 = 2, K1_W256 = 3, K1_L32M = 4, 
 hipError_t launch_k1(int bf16, int dma, int layout, int kc, dim3 grid, const K1Args& a, hipStream_t st);
 hipError_t launch_zero_u32(uint32_t* p, int n, hipStream_t st);
 
-// ---------------------------------------------------------------- K2
-struct K2Args {
-  const float2* stats;
-  const int2* lists;
-  int P, N, V, k, S;
-  const float* prev;
-  const int32_t* off;
-  int32_t* tok;
-  int32_t* par;
-  float* score;
-  float* row_lse;     // nullable
-};
-
-hipError_t launch_k2(const K2Args& a, hipStream_t st);
-hipError_t launch_add_word_base(int2* lists, size_t n, int base, int v_shard, hipStream_t st);
-hipError_t launch_k2_argmax(const int2* lists, int P, int N, int32_t* tok, float* val, hipStream_t st);
-
-// ---------------------------------------------------------------- K3 / gather
-hipError_t launch_compact(int S, int k, const uint8_t* alive, int32_t* keep, int32_t* kept_count,
-                          int32_t* new_off, int32_t* kept_sent, int32_t* new_S, hipStream_t st);
-
-hipError_t launch_gather(int n_max, const int32_t* n_dev, const int32_t* idx, const void* src,
-                         void* dst, size_t row_bytes, hipStream_t st);
-
-// ---------------------------------------------------------------- unfused baseline
-hipError_t launch_k1_wide_store(dim3 grid, const K1Args& a, hipStream_t st);
-hipError_t launch_uf_add_bias(float* x, const float* b, int N, int V, hipStream_t st);
-hipError_t launch_uf_softmax3(float* x, int N, int V, float* row_lse, hipStream_t st);
-hipError_t launch_uf_kbest_rows(const float* p, int N, int V, int k, float2* stats, int2* lists, hipStream_t st);
-hipError_t launch_uf_fused_rows(const float* x, const float* b, int N, int V, int k, float2* stats, int2* lists,
-                                hipStream_t st);
-
-// ---------------------------------------------------------------- per-hypothesis EOS
-hipError_t launch_beam_finish(int S, int k, int t, int T, int eos, const int32_t* token, const int32_t* parent,
-                              const float* score, const int32_t* sid, int32_t* beam, const int32_t* prev_keep,
-                              int prev_hist_base, int hist_base, int32_t* hist_token, int32_t* hist_parent,
-                              int32_t* fin_count, float* fin_score, int32_t* fin_len, int32_t* fin_hist,
-                              uint8_t* alive, hipStream_t st);
-hipError_t launch_beam_backtrace(int S0, int k, int T, float alpha, const int32_t* fin_count, const float* fin_score,
-                                 const int32_t* fin_len, const int32_t* fin_hist, const int32_t* hist_token,
-                                 const int32_t* hist_parent, int32_t* out_tokens, int32_t* out_len,
-                                 float* out_score, float* out_norm, hipStream_t st);
-
-// ---------------------------------------------------------------- decoder stand-in
-hipError_t launch_standin_alive(int S, int k, int t, const int32_t* sid, const int32_t* lengths, uint8_t* alive,
-                                hipStream_t st);
-hipError_t launch_standin_next_h(int n_max, const int32_t* n_dev, int k, int T, int t, const int32_t* keep,
-                                 const int32_t* sid, const void* table, void* out, size_t row_bytes,
-                                 hipStream_t st);
-
 }  // namespace kb

@@ -8,7 +8,7 @@
 
 #include "kbest.h"
 #include "kbest_standin.h"
-#include "kb_common.hpp"
+#include "kb_launch.hpp"
 
 namespace kb {
 hipError_t launch_k1_reg_bf16_L256(int kc, dim3 grid, const K1Args& a, hipStream_t st);

@@ -8,7 +8,7 @@
 //     reaches its drawn length this step (every continuation ends together);
 //   * standin_next_h: the next step's state of each surviving entry, read
 //     from the table at (original sentence id, step, beam slot).
-#include "kb_common.hpp"
+#include "kb_launch.hpp"
 
 namespace kb {
 

@@ -12,7 +12,7 @@
 // The projection is the 256 x 256 MFMA kernel with a store epilogue; the beam
 // merge is K2 with a single "split" per row.  The row kernels use one
 // 256-thread workgroup per row.
-#include "kb_common.hpp"
+#include "kb_launch.hpp"
 
 namespace kb {
 
