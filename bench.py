@@ -274,6 +274,85 @@ def ablation_bench(torch, np, kb, reps: int = 10):
             "reps": reps, "rows": rows, "greedy_beam1": greedy, "precision": prec}
 
 
+PEAK_F32_TFLOPS = 157.3
+
+
+def configs_bench(torch, np, kb, reps: int = 50):
+    """Every single-step workload (the decode-loop one is timed by the loop):
+    warm steps back to back (median and min of per-step HIP events), cold steps
+    after a 512 MB write, the projection kernel alone, its roofline, and the
+    fp64 oracle on the whole workload beside it (on the host's cores)."""
+    from oracle import kbest_oracle as ko
+    from synth import workloads as wl
+    res = []
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    ev = HipEvents()
+    stream = torch.cuda.current_stream().cuda_stream
+    for c in wl.WORKLOADS[:4]:
+        inp = wl.make_workload(c["name"])
+        N, H, V, k, S = inp.N, inp.H, inp.V, inp.k, inp.S
+        if inp.dtype == "bf16":
+            h, W, b, prev, off = to_dev(inp, torch, np)
+        else:
+            h, W = torch.from_numpy(inp.h).cuda(), torch.from_numpy(inp.W).cuda()
+            b, prev, off = (torch.from_numpy(x).cuda() for x in (inp.b, inp.prev, inp.off))
+        dt = kb.KB_BF16 if inp.dtype == "bf16" else kb.KB_F32
+        out = tuple(torch.empty((S, k), dtype=t, device="cuda") for t in (torch.int32, torch.int32, torch.float32))
+        ws = kb.workspace(kb.kbest_workspace_bytes(dt, N, H, V, k, S))
+        step = lambda events=None: kb.kbest_step(h, W, b, prev, off, k, out=out, ws=ws, events=events)
+        for _ in range(10):
+            step()
+        torch.cuda.synchronize()
+        pairs = [(ev.create(), ev.create()) for _ in range(reps)]
+        for i in range(reps):              # warm: per-step events around the whole call
+            ev.record(pairs[i][0], stream)
+            step()
+            ev.record(pairs[i][1], stream)
+        torch.cuda.synchronize()
+        warm = sorted(ev.elapsed_ms(x, y) for x, y in pairs)
+        for i in range(reps):              # the projection kernel alone
+            step(events=pairs[i])
+        torch.cuda.synchronize()
+        kern = sorted(ev.elapsed_ms(x, y) for x, y in pairs)
+        cold = []
+        for i in range(10):
+            flush.fill_(1)
+            ev.record(pairs[i][0], stream)
+            step()
+            ev.record(pairs[i][1], stream)
+            torch.cuda.synchronize()
+            cold.append(ev.elapsed_ms(*pairs[i]))
+        cold.sort()
+        for x, y in pairs:
+            ev.destroy(x)
+            ev.destroy(y)
+        esz = 2 if inp.dtype == "bf16" else 4
+        nbytes = H * V * esz + N * H * esz + V * 4 + N * 4 + S * k * 12
+        flops = 2.0 * N * H * V
+        km = kern[len(kern) // 2]
+        if flops / nbytes < (PEAK_BF16_TFLOPS if inp.dtype == "bf16" else PEAK_F32_TFLOPS) * 1e12 / (PEAK_HBM_GBS * 1e9):
+            roof = {"bound": "hbm", "achieved": nbytes / (km * 1e-3) / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+        else:
+            pk = PEAK_BF16_TFLOPS if inp.dtype == "bf16" else PEAK_F32_TFLOPS
+            roof = {"bound": "mfma", "achieved": flops / (km * 1e-3) / 1e12, "peak": pk, "unit": "TFLOP/s"}
+        roof["frac"] = roof["achieved"] / roof["peak"]
+        t0 = time.perf_counter()
+        orc_runs = 10 if N * V < 1e6 else 1
+        whole = N * V < 1e8               # the V=90k workload's oracle is timed on a sample by the main bench
+        for _ in range(orc_runs if whole else 0):
+            ko.kbest_step(inp.h, inp.W, inp.b, inp.prev, inp.off, k, dtype=inp.dtype)
+        orc = (time.perf_counter() - t0) / orc_runs if whole else None
+        res.append({"workload": inp.name, "N": N, "H": H, "V": V, "k": k, "dtype": inp.dtype,
+                    "step_ms_median": warm[len(warm) // 2], "step_ms_min": warm[0],
+                    "cold_step_ms_median": cold[len(cold) // 2], "kernel_ms_median": km,
+                    "hyps_per_s": N / (warm[len(warm) // 2] * 1e-3), "roofline": roof,
+                    "oracle_s": orc, "oracle_hyps_per_s": (N / orc) if orc else None})
+        log(f"{inp.name}: step {warm[len(warm) // 2]:.4f} ms, kernel {km:.4f} ms, {roof['bound']} "
+            f"{roof['frac'] * 100:.1f}%, oracle {orc}")
+    del flush
+    return res
+
+
 def shard_bench(torch, np, kb, reps: int = 20):
     """One device's part of a vocabulary-split step (Algorithm 6 across devices):
     the V=90k workload cut into 8 shards on multiples of 8 words; each shard's
@@ -448,6 +527,9 @@ def main():
     ap.add_argument("--sweep", action="store_true",
                     help="only run the row-count and batch-size sweeps and the per-step curves of a "
                          "1280-sentence decode, print them as the JSON line and exit")
+    ap.add_argument("--configs", action="store_true",
+                    help="only time every single-step workload (warm, cold, kernel, roofline, oracle beside it), "
+                         "print that as the JSON line and exit")
     ap.add_argument("--shards", action="store_true",
                     help="only time one device's part of a step split over 8 vocabulary shards (each shard's "
                          "projection and the merge of all partials) at V=90k, print it as the JSON line and exit")
@@ -480,6 +562,12 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "launches": 3}))
+        return
+    if args.configs:
+        kb.lib()
+        res = {"metric": "step time per workload", "unit": "ms", "data": "synthetic (seeded)", "n_gpus": 1,
+               "configs": configs_bench(torch, np, kb)}
+        print(json.dumps(res), flush=True)
         return
     if args.shards:
         kb.lib()
