@@ -43,7 +43,7 @@ extern "C" {
 typedef enum kb_status {
   KB_OK = 0,
   KB_ERR_INVALID_ARG = 1, /* null pointer, bad size, k out of range, ... */
-  KB_ERR_UNSUPPORTED = 2, /* a valid request this build does not handle  */
+  KB_ERR_UNSUPPORTED = 2, /* a valid request the library does not handle */
   KB_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required  */
   KB_ERR_HIP = 4          /* a HIP launch failed; see kb_last_error()     */
 } kb_status;
