@@ -101,9 +101,13 @@ size_t kb_kbest_workspace_bytes(int dtype, int N, int H, int V, int k, int S);
  *   W             H x V row-major (V contiguous), element type `dtype`.
  *   b             V float32 bias.
  *   prev_score    N float32 cumulative log-probability of each row.
- *   sent_offsets  S+1 int32 (the beam map): 0 = off[0] < off[1] < ... <
- *                 off[S] = N; every sentence owns at least one row.  Device
- *                 contents are trusted (not checked).
+ *   sent_offsets  S+1 int32 (the beam map): 0 = off[0] <= off[1] <= ... <=
+ *                 off[S] <= N; sentence s owns rows off[s] .. off[s+1] - 1.
+ *                 A sentence with no rows gets k entries with token and
+ *                 parent -1 and score -inf; rows from off[S] on are projected
+ *                 but belong to no sentence (a step sized by an upper bound,
+ *                 see kb_compact_batch).  Device contents are trusted (not
+ *                 checked).
  *   out_token     S x k int32: word index in [0, V).
  *   out_parent    S x k int32: global row index of the parent hypothesis.
  *   out_score     S x k float32: cumulative log-probability, descending.
@@ -201,7 +205,11 @@ int kb_kbest_step_unfused(int mode, int dtype, int N, int H, int V, int k, int S
  *   kept_count        device int32 scalar: number of surviving entries.
  *   new_sent_offsets  nullable, S+1 int32: the first *new_S + 1 entries are
  *                     the row offsets of the compacted batch (sentences with
- *                     no surviving entry are dropped).
+ *                     no surviving entry are dropped); entries *new_S + 1 .. S
+ *                     repeat *kept_count, so a step launched for more
+ *                     sentences than survive (an upper bound known on the
+ *                     host before the counts are) sees only empty sentences
+ *                     past *new_S.
  *   kept_sentence     nullable, S int32: for each surviving sentence, its
  *                     index in the old batch.
  *   new_S             nullable, device int32 scalar: surviving sentences.

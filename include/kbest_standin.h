@@ -22,17 +22,21 @@ extern "C" {
 #endif
 
 /*
- * kb_standin_alive -- alive[s*k + r] = (t < lengths[sid[s]] - 1) ? 1 : 0 for
- * s < S, r < k: the batch entries that stay after step t, when sentence s
- * (original id sid[s]) emits EOS on every continuation at step
- * lengths[sid[s]] - 1.
+ * kb_standin_alive -- alive[s*k + r] = (s < S_live && t < lengths[sid[s]] - 1)
+ * ? 1 : 0 for s < S, r < k: the batch entries that stay after step t, when
+ * sentence s (original id sid[s]) emits EOS on every continuation at step
+ * lengths[sid[s]] - 1.  S_live = min(S, *S_dev), or S if S_dev is NULL: a
+ * loop that sizes a step by an upper bound S on the sentence count passes the
+ * exact count on the device, and the entries of sentences past it are 0 (sid
+ * is not read for them).
+ *   S_dev    NULL or one int32 on the device (e.g. kb_compact_batch's new_S).
  *   sid      S int32, original sentence ids (indices into lengths).
  *   lengths  int32 per original sentence.
  *   alive    S*k uint8 output, the input of kb_compact_batch.
  * S == 0 is a no-op.  0 <= S, 1 <= k, S*k fits in int32.
  */
-int kb_standin_alive(int S, int k, int t, const int32_t* sid, const int32_t* lengths, uint8_t* alive,
-                     void* stream);
+int kb_standin_alive(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
+                     uint8_t* alive, void* stream);
 
 /*
  * kb_standin_next_h -- the states of step t for the entries kept by

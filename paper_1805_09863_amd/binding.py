@@ -48,7 +48,7 @@ SIGNATURES = {
     "kb_shard_partials": (_I, [_I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "kb_merge_partials": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     # decoder stand-in of the synthetic decode loop (include/kbest_standin.h)
-    "kb_standin_alive": (_I, [_I, _I, _I, _P, _P, _P, _P]),
+    "kb_standin_alive": (_I, [_I, _P, _I, _I, _P, _P, _P, _P]),
     "kb_standin_next_h": (_I, [_I, _P, _I, _I, _I, _P, _P, _P, _P, _SZ, _P]),
 }
 
@@ -335,9 +335,10 @@ def merge_partials(stats: torch.Tensor, lists: torch.Tensor, P: int, V: int, k: 
 
 
 def standin_alive(sid: torch.Tensor, lengths: torch.Tensor, S: int, k: int, t: int, *, out: torch.Tensor,
-                  stream=None) -> torch.Tensor:
-    """out[s*k + r] = (t < lengths[sid[s]] - 1) for s < S (include/kbest_standin.h)."""
-    _check(lib().kb_standin_alive(S, k, t, _ptr(sid), _ptr(lengths), _ptr(out), _stream(stream)))
+                  S_dev: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """out[s*k + r] = (s < min(S, S_dev[0]) and t < lengths[sid[s]] - 1) for s < S
+    (include/kbest_standin.h)."""
+    _check(lib().kb_standin_alive(S, _ptr(S_dev), k, t, _ptr(sid), _ptr(lengths), _ptr(out), _stream(stream)))
     return out
 
 

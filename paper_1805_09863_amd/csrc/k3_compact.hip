@@ -83,10 +83,11 @@ __global__ __launch_bounds__(K3_T) void k3_compact(int S, int k, const uint8_t* 
     sbase += total >> 20;
     ebase += total & 0xFFFFF;
   }
-  if (tid == 0) {
-    if (new_off) new_off[sbase] = ebase;
-    if (new_S) *new_S = sbase;
-  }
+  // the end of the last surviving sentence, repeated up to entry S: a launch
+  // sized for more sentences than survive sees only empty ones past new_S
+  if (new_off)
+    for (int s = sbase + tid; s <= S; s += K3_T) new_off[s] = ebase;
+  if (tid == 0 && new_S) *new_S = sbase;
 }
 
 hipError_t launch_compact(int S, int k, const uint8_t* alive, int32_t* keep, int32_t* kept_count,

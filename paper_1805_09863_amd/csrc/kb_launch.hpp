@@ -52,8 +52,8 @@ hipError_t launch_beam_backtrace(int S0, int k, int T, float alpha, const int32_
                                  float* out_score, float* out_norm, hipStream_t st);
 
 // ---------------------------------------------------------------- decoder stand-in
-hipError_t launch_standin_alive(int S, int k, int t, const int32_t* sid, const int32_t* lengths, uint8_t* alive,
-                                hipStream_t st);
+hipError_t launch_standin_alive(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
+                                uint8_t* alive, hipStream_t st);
 hipError_t launch_standin_next_h(int n_max, const int32_t* n_dev, int k, int T, int t, const int32_t* keep,
                                  const int32_t* sid, const void* table, void* out, size_t row_bytes,
                                  hipStream_t st);

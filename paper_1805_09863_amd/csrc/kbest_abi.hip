@@ -168,7 +168,7 @@ int validate_step(int dtype, int N, int H, int V, int k, int S) {
   if (H < 1 || V < 1) return fail(KB_ERR_INVALID_ARG, "H = %d and V = %d must be >= 1", H, V);
   if (k < 1 || k > KB_MAX_K || k > V)
     return fail(KB_ERR_INVALID_ARG, "k = %d outside [1, min(%d, V = %d)]", k, KB_MAX_K, V);
-  if (N < S) return fail(KB_ERR_INVALID_ARG, "N = %d < S = %d: every sentence needs a row", N, S);
+  if (N < S) return fail(KB_ERR_INVALID_ARG, "N = %d < S = %d: N >= S is required", N, S);
   if ((long long)N * k > INT_MAX || (long long)S * k > INT_MAX || (long long)H * V > (1LL << 40))
     return fail(KB_ERR_UNSUPPORTED, "shape too large");
   if ((long long)N * V > (1LL << 46)) return fail(KB_ERR_UNSUPPORTED, "N * V too large");
@@ -562,7 +562,7 @@ int kb_merge_partials(int N, int V, int k, int S, int P, const float* stats, con
                       float* out_score, float* out_row_lse, void* stream) {
   if (N < 0 || S < 0) return fail(KB_ERR_INVALID_ARG, "negative N (%d) or S (%d)", N, S);
   if ((N == 0) != (S == 0)) return fail(KB_ERR_INVALID_ARG, "N = %d and S = %d: both or neither must be 0", N, S);
-  if (N < S) return fail(KB_ERR_INVALID_ARG, "N = %d < S = %d: every sentence needs a row", N, S);
+  if (N < S) return fail(KB_ERR_INVALID_ARG, "N = %d < S = %d: N >= S is required", N, S);
   if (V < 1) return fail(KB_ERR_INVALID_ARG, "V = %d must be >= 1", V);
   if (k < 1 || k > KB_MAX_K || k > V) return fail(KB_ERR_INVALID_ARG, "k = %d outside [1, min(%d, V = %d)]", k, KB_MAX_K, V);
   if (P < 1 || P > 256) return fail(KB_ERR_UNSUPPORTED, "P = %d splits outside [1, 256]", P);
@@ -590,13 +590,14 @@ int kb_merge_partials(int N, int V, int k, int S, int P, const float* stats, con
   return ok();
 }
 
-int kb_standin_alive(int S, int k, int t, const int32_t* sid, const int32_t* lengths, uint8_t* alive,
-                     void* stream) {
+int kb_standin_alive(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
+                     uint8_t* alive, void* stream) {
   if (S < 0 || k < 1) return fail(KB_ERR_INVALID_ARG, "S = %d, k = %d", S, k);
   if ((long long)S * k > INT_MAX) return fail(KB_ERR_UNSUPPORTED, "S*k does not fit in int32");
   if (S == 0) return ok();
   if (!sid || !lengths || !alive) return fail(KB_ERR_INVALID_ARG, "null sid, lengths or alive");
-  hipError_t e = kb::launch_standin_alive(S, k, t, sid, lengths, alive, reinterpret_cast<hipStream_t>(stream));
+  hipError_t e = kb::launch_standin_alive(S, S_dev, k, t, sid, lengths, alive,
+                                          reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(KB_ERR_HIP, "stand-in alive kernel launch: %s", hipGetErrorString(e));
   return ok();
 }

@@ -12,12 +12,16 @@
 
 namespace kb {
 
-__global__ __launch_bounds__(256) void standin_alive(int S, int k, int t, const int32_t* __restrict__ sid,
+__global__ __launch_bounds__(256) void standin_alive(int S, const int32_t* __restrict__ S_dev, int k, int t,
+                                                     const int32_t* __restrict__ sid,
                                                      const int32_t* __restrict__ lengths,
                                                      uint8_t* __restrict__ alive) {
   const int n = S * k;
-  for (int e = blockIdx.x * 256 + threadIdx.x; e < n; e += gridDim.x * 256)
-    alive[e] = t < lengths[sid[e / k]] - 1 ? 1 : 0;
+  const int live = S_dev ? min(S, *S_dev) : S;  // sentences past it do not exist this step
+  for (int e = blockIdx.x * 256 + threadIdx.x; e < n; e += gridDim.x * 256) {
+    const int s = e / k;
+    alive[e] = (s < live && t < lengths[sid[s]] - 1) ? 1 : 0;
+  }
 }
 
 template <class V>
@@ -36,11 +40,11 @@ __global__ __launch_bounds__(256) void standin_next_h(int n_max, const int32_t* 
   }
 }
 
-hipError_t launch_standin_alive(int S, int k, int t, const int32_t* sid, const int32_t* lengths, uint8_t* alive,
-                                hipStream_t st) {
+hipError_t launch_standin_alive(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
+                                uint8_t* alive, hipStream_t st) {
   const int n = S * k;
   const int blocks = n > 0 ? min((n + 255) / 256, 1024) : 1;
-  standin_alive<<<dim3(blocks), dim3(256), 0, st>>>(S, k, t, sid, lengths, alive);
+  standin_alive<<<dim3(blocks), dim3(256), 0, st>>>(S, S_dev, k, t, sid, lengths, alive);
   return hipGetLastError();
 }
 

@@ -22,8 +22,9 @@ from . import binding as kbb
 @dataclass
 class LoopStats:
     steps: int = 0
-    rows: list = field(default_factory=list)     # live rows decoded at each step
+    rows: list = field(default_factory=list)         # live rows decoded at each step
     total_rows: int = 0
+    launch_rows: list = field(default_factory=list)  # rows each launch was sized for (compacted loop)
 
 
 def decode_loop(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, lengths: torch.Tensor,
@@ -44,12 +45,22 @@ def decode_loop(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, lengths
 
     A compacted step enqueues the output layer, the stand-in's EOS mask, the
     compaction, the gathers of the surviving scores and sentence ids and the
-    stand-in's next states, then waits for the two counts (rows, sentences)
-    that size the next step's launch: one host synchronisation per step,
-    after all of the step's work is queued.
+    stand-in's next states.  The batch only shrinks, so step t + 1 is launched
+    sized by the exact counts of step t (rows, sentences), read from the
+    device while step t is still queued: the host never waits for the step it
+    has just launched, and the device never waits for the host.  Every kernel
+    of a step takes the exact counts of its own batch from the device (the
+    compaction's outputs); rows and sentences past them are launched but
+    empty, since the compaction pads the sentence offsets past its last kept
+    sentence.  The price is a few rows of the sentences that ended at the step
+    before, and one launch at the end whose batch turns out to be empty.
 
-    ``on_step(t, state)`` is called after each output-layer step with a dict
-    of the device tensors of that step.
+    ``on_step(t, state)`` is called once step t's work is queued, with a dict
+    of the device tensors of that step cut to its exact counts; work that
+    on_step queues on ``stream`` sees them complete, and they stay intact
+    until on_step returns.  In the compacted loop ``S_launch`` and
+    ``N_launch`` give the sizes the step was launched with, ``token_launch``
+    and ``score_launch`` its whole outputs.
     """
     dev = W.device
     beam = k
@@ -83,38 +94,55 @@ def decode_loop(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, lengths
     if compact:
         alive = torch.empty(M0, dtype=torch.uint8, device=dev)
         keep = torch.empty(M0, **i32)
-        cnt = torch.empty(2, **i32)                      # kept rows, kept sentences
         noff = torch.empty(S0 + 1, **i32)
         ksent = torch.empty(S0, **i32)
-        prev_nx = torch.empty(M0, dtype=torch.float32, device=dev)
+        # rows past a step's exact count are projected: keep them finite
+        h_nx = torch.zeros((M0, H), dtype=h_table.dtype, device=dev)
+        prev_nx = torch.zeros(M0, dtype=torch.float32, device=dev)
         sid_nx = torch.empty(S0, **i32)
-        cnt_host = torch.empty(2, dtype=torch.int32, pin_memory=True)
-        ready = torch.cuda.Event()
-        while S > 0:
+        # counts (kept rows, kept sentences) of each step, double-buffered on
+        # both sides: step t writes slot t % 2, read back one step later
+        cnt = [torch.empty(2, **i32) for _ in range(2)]
+        cnt_host = [torch.empty(2, dtype=torch.int32, pin_memory=True) for _ in range(2)]
+        ready = [torch.cuda.Event(), torch.cuda.Event()]
+        S_ex = None                                      # the device's count of the current batch's sentences
+        while t < T:
+            c = cnt[t % 2]
             kbb.kbest_step(h_cur[:N], W, b, prev[:N], off[:S + 1], k, S=S,
                            out=(tok[:S * k].view(S, k), par[:S * k].view(S, k), sc[:S * k].view(S, k)),
                            ws=ws, stream=stream)
-            stats.rows.append(N)
-            if on_step is not None:
-                on_step(t, dict(h=h_cur[:N], prev=prev[:N], off=off[:S + 1], sid=sid[:S],
-                                token=tok[:S * k].view(S, k), parent=par[:S * k].view(S, k),
-                                score=sc[:S * k].view(S, k), S=S, N=N))
-            kbb.standin_alive(sid, lengths, S, k, t, out=alive, stream=stream)
-            kbb.compact_batch(alive[:S * k], S, k, out=(keep, cnt[0:1], noff, ksent, cnt[1:2]), stream=stream)
-            cnt_host.copy_(cnt, non_blocking=True)
-            ready.record(stream)
-            kbb.gather_rows(sc[:S * k].view(S * k, 1), keep, n_dev=cnt[0:1], n_max=S * k,
+            kbb.standin_alive(sid, lengths, S, k, t, out=alive, S_dev=S_ex, stream=stream)
+            kbb.compact_batch(alive[:S * k], S, k, out=(keep, c[0:1], noff, ksent, c[1:2]), stream=stream)
+            cnt_host[t % 2].copy_(c, non_blocking=True)
+            ready[t % 2].record(stream)
+            kbb.gather_rows(sc[:S * k].view(S * k, 1), keep, n_dev=c[0:1], n_max=S * k,
                             out=prev_nx.view(M0, 1), stream=stream)
-            kbb.gather_rows(sid[:S].view(S, 1), ksent, n_dev=cnt[1:2], n_max=S, out=sid_nx.view(S0, 1),
+            kbb.gather_rows(sid[:S].view(S, 1), ksent, n_dev=c[1:2], n_max=S, out=sid_nx.view(S0, 1),
                             stream=stream)
             if t + 1 < T:
-                kbb.standin_next_h(h_table, keep, sid, k, T, t + 1, S * k, n_dev=cnt[0:1], out=h_cur,
+                kbb.standin_next_h(h_table, keep, sid, k, T, t + 1, S * k, n_dev=c[0:1], out=h_nx,
                                    stream=stream)
-            ready.synchronize()                            # the step's one host sync
-            N, S = (int(x) for x in cnt_host.tolist())
+            stats.launch_rows.append(N)
+            # the exact counts of this step's batch: the previous step's output
+            if t == 0:
+                N_ex, S_now = M0, S0
+            else:
+                ready[(t - 1) % 2].synchronize()
+                N_ex, S_now = (int(x) for x in cnt_host[(t - 1) % 2].tolist())
+            if N_ex == 0:
+                break                                    # every sentence had ended: this launch was empty
+            stats.rows.append(N_ex)
+            if on_step is not None:
+                on_step(t, dict(h=h_cur[:N_ex], prev=prev[:N_ex], off=off[:S_now + 1], sid=sid[:S_now],
+                                token=tok[:S_now * k].view(S_now, k), parent=par[:S_now * k].view(S_now, k),
+                                score=sc[:S_now * k].view(S_now, k), S=S_now, N=N_ex, S_launch=S, N_launch=N,
+                                token_launch=tok[:S * k].view(S, k), score_launch=sc[:S * k].view(S, k)))
+            N, S = N_ex, S_now                           # bounds of the next step's batch
+            S_ex = c[1:2]
             prev, prev_nx = prev_nx, prev
             sid, sid_nx = sid_nx, sid
             off, noff = noff, off
+            h_cur, h_nx = h_nx, h_cur
             t += 1
     else:
         while t < Lmax:

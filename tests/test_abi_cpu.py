@@ -37,11 +37,11 @@ def test_library_exports_every_declared_function(repo_root):
 
 def test_standin_argument_checks():
     L = binding.lib()
-    assert L.kb_standin_alive(0, 5, 0, None, None, None, None) == KB_OK            # empty batch: no-op
-    assert L.kb_standin_alive(-1, 5, 0, FAKE, FAKE, FAKE, None) == KB_ERR_INVALID_ARG
-    assert L.kb_standin_alive(3, 0, 0, FAKE, FAKE, FAKE, None) == KB_ERR_INVALID_ARG
-    assert L.kb_standin_alive(3, 5, 0, None, FAKE, FAKE, None) == KB_ERR_INVALID_ARG
-    assert L.kb_standin_alive(1 << 30, 4, 0, FAKE, FAKE, FAKE, None) == KB_ERR_UNSUPPORTED
+    assert L.kb_standin_alive(0, None, 5, 0, None, None, None, None) == KB_OK            # empty batch: no-op
+    assert L.kb_standin_alive(-1, None, 5, 0, FAKE, FAKE, FAKE, None) == KB_ERR_INVALID_ARG
+    assert L.kb_standin_alive(3, None, 0, 0, FAKE, FAKE, FAKE, None) == KB_ERR_INVALID_ARG
+    assert L.kb_standin_alive(3, None, 5, 0, None, FAKE, FAKE, None) == KB_ERR_INVALID_ARG
+    assert L.kb_standin_alive(1 << 30, None, 4, 0, FAKE, FAKE, FAKE, None) == KB_ERR_UNSUPPORTED
     nh = L.kb_standin_next_h
     assert nh(0, None, 5, 60, 1, FAKE, FAKE, FAKE, FAKE, 2048, None) == KB_OK        # nothing to gather
     assert nh(4, None, 5, 60, 60, FAKE, FAKE, FAKE, FAKE, 2048, None) == KB_ERR_INVALID_ARG   # t >= T

@@ -57,6 +57,8 @@ def test_compact_bit_exact(kb, pattern, S, k):
     ns = int(nS.item())
     assert ns == ref.new_S
     assert np.array_equal(noff.cpu().numpy()[:ns + 1], ref.new_offsets)
+    # past the kept sentences the offsets repeat the kept count (empty sentences)
+    assert (noff.cpu().numpy()[ns + 1:S + 1] == n).all()
     assert np.array_equal(ksent.cpu().numpy()[:ns], ref.kept_sentence)
 
 
@@ -84,3 +86,24 @@ def test_gather_rows(kb, row_elems, dtype):
     want = src[idx[:150].long()]
     assert torch.equal(out[:150], want)
     assert torch.count_nonzero(out[150:]) == 0
+
+
+@pytest.mark.parametrize("S_live", [None, 0, 1, 9, 20, 25])
+def test_standin_alive_device_count(kb, S_live):
+    # EOS mask of the decoder stand-in: entries of sentences at or past the
+    # device count are 0 and their (stale) sentence ids are never read
+    S, k, t = 20, 3, 4
+    g = np.random.default_rng(77)
+    lengths = g.integers(1, 9, 50).astype(np.int32)
+    lengths[49] = 8                               # alive at step t
+    sid = g.permutation(49)[:S].astype(np.int32)
+    live = S if S_live is None else min(S, S_live)
+    sid_dev = torch.from_numpy(sid).cuda()
+    sid_dev[live:] = 49                           # stale ids: would read as alive
+    alive = torch.full((S * k,), 7, dtype=torch.uint8, device="cuda")
+    s_dev = None if S_live is None else torch.tensor([S_live], dtype=torch.int32, device="cuda")
+    from paper_1805_09863_amd import binding as kbb
+    kbb.standin_alive(sid_dev, torch.from_numpy(lengths).cuda(), S, k, t, out=alive, S_dev=s_dev)
+    torch.cuda.synchronize()
+    want = np.repeat((np.arange(S) < live) & (t < lengths[sid] - 1), k).astype(np.uint8)
+    assert np.array_equal(alive.cpu().numpy(), want)

@@ -43,11 +43,17 @@ def _run(kb, work, sample_per_step):
     k = work.k
     S0 = work.S
     g = np.random.default_rng(9)
-    checked = {"oracle": 0, "naive": 0, "steps": 0}
+    checked = {"oracle": 0, "naive": 0, "steps": 0, "padded": 0}
 
     def on_step(t, st):
         S, N = st["S"], st["N"]
         checked["steps"] += 1
+        # launched for the previous step's counts: the sentences past this
+        # step's batch came out empty
+        assert st["S_launch"] >= S and st["N_launch"] >= N
+        assert (st["token_launch"][S:] == -1).all()
+        assert torch.isneginf(st["score_launch"][S:]).all()
+        checked["padded"] += st["S_launch"] - S
         tok, par, sc = (x.cpu().numpy() for x in (st["token"], st["parent"], st["score"]))
         off = st["off"].cpu().numpy()
         sid = st["sid"].cpu().numpy()
@@ -86,6 +92,10 @@ def _run(kb, work, sample_per_step):
     stats = decode_loop(h_table, W, b, L, p0, k, work.T, compact=True, on_step=on_step)
     want_rows = [k * int((work.lengths > t).sum()) for t in range(int(work.lengths.max()))]
     assert stats.rows == want_rows
+    # step t is launched sized by step t - 1's batch; a last, empty launch
+    # follows when the longest sentence ends before T
+    assert stats.launch_rows[:len(want_rows)] == want_rows[:1] + want_rows[:-1]
+    assert stats.launch_rows[len(want_rows):] == ([want_rows[-1]] if len(want_rows) < work.T else [])
     naive = decode_loop(h_table, W, b, L, p0, k, work.T, compact=False)
     assert naive.steps == stats.steps == int(work.lengths.max())
     assert naive.total_rows == stats.total_rows

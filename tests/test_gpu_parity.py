@@ -9,7 +9,7 @@ import pytest
 import torch
 
 from synth import workloads as wl
-from tests.gpu_util import check, run_step, say
+from tests.gpu_util import check, run_step, say, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -179,6 +179,32 @@ def test_empty_batch_is_a_no_op(kb):
     keep, kept, noff, ksent, nS = kb.compact_batch(torch.empty(0, dtype=torch.uint8, device="cuda"), 0, 5)
     torch.cuda.synchronize()
     assert int(kept.item()) == 0 and int(nS.item()) == 0 and int(noff[0].item()) == 0
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_empty_sentences_and_rows_past_the_batch(kb, dt):
+    # a step launched for more sentences and rows than it holds (a decode loop
+    # sized by the previous step's counts): empty sentences between and after
+    # the real ones, and rows after off[S] that belong to no sentence
+    rps = [3, 5, 2, 4, 1]
+    inp = wl.make_step(H=128, V=9000, k=6, rows_per_sentence=rps, dtype=dt, seed=901, name=f"holes_{dt}")
+    h, W, b, prev, _ = to_dev(inp)
+    extra = 9
+    junk = torch.randn((extra, inp.H), device="cuda").to(h.dtype) * 4
+    h = torch.cat([h, junk]).contiguous()
+    prev = torch.cat([prev, torch.zeros(extra, device="cuda")]).contiguous()
+    layout = [0, 3, 0, 5, 0, 0, 2, 4, 1, 0, 0]        # sentence sizes; the zeros are empty sentences
+    real = [i for i, n in enumerate(layout) if n > 0]
+    off = torch.tensor(np.concatenate([[0], np.cumsum(layout)]).astype(np.int32), device="cuda")
+    S = len(layout)
+    tok, par, sc = kb.kbest_step(h, W, b, prev, off, inp.k, S=S)
+    torch.cuda.synchronize()
+    tok, par, sc = tok.cpu().numpy(), par.cpu().numpy(), sc.cpu().numpy()
+    empty = [i for i in range(S) if i not in real]
+    assert (tok[empty] == -1).all() and (par[empty] == -1).all() and np.isneginf(sc[empty]).all()
+    say(f"{inp.N} rows + {extra} past the batch, {len(empty)} empty sentences of {S}")
+    rep, _ = check(inp, (tok[real], par[real], sc[real]))
+    say(f"  max score err {rep.max_score_err:.2e}, {rep.n_checked_idx} exact ranks")
 
 
 def test_deterministic_and_workspace_poison(kb):
