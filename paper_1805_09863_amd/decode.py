@@ -88,7 +88,7 @@ def decode_loop(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, lengths
     ident = torch.arange(M0, **i32)                      # entry e of an S0 x k batch is row e
     sid = torch.arange(S0, **i32)                        # original id of each live sentence
     off = (torch.arange(S0 + 1, **i32) * beam).contiguous()
-    prev = prev0.to(torch.float32).contiguous()
+    prev = prev0.to(device=dev, dtype=torch.float32, copy=True).contiguous()   # the loop writes its own
     kbb.standin_next_h(h_table, ident, sid, k, T, 0, M0, out=h_cur, stream=stream)
     S, N, t = S0, M0, 0
     if compact:
@@ -113,7 +113,8 @@ def decode_loop(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, lengths
                            ws=ws, stream=stream)
             kbb.standin_alive(sid, lengths, S, k, t, out=alive, S_dev=S_ex, stream=stream)
             kbb.compact_batch(alive[:S * k], S, k, out=(keep, c[0:1], noff, ksent, c[1:2]), stream=stream)
-            cnt_host[t % 2].copy_(c, non_blocking=True)
+            with torch.cuda.stream(stream):              # the copy runs on the loop's stream
+                cnt_host[t % 2].copy_(c, non_blocking=True)
             ready[t % 2].record(stream)
             kbb.gather_rows(sc[:S * k].view(S * k, 1), keep, n_dev=c[0:1], n_max=S * k,
                             out=prev_nx.view(M0, 1), stream=stream)
@@ -241,7 +242,8 @@ def beam_search(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, k: int,
                             prev_keep=keep[1 - cur][:N] if t > 0 else None, prev_base=prev_base, base=base,
                             hist_token=hist_tok, hist_parent=hist_par, fin=fin, S=S, N=N))
         kbb.compact_batch(alive[:S * k], S, k, out=(keep[cur], cnt[0:1], noff, ksent, cnt[1:2]), stream=stream)
-        cnt_host.copy_(cnt, non_blocking=True)
+        with torch.cuda.stream(stream):                # the copy runs on the loop's stream
+            cnt_host.copy_(cnt, non_blocking=True)
         ready.record(stream)
         kbb.gather_rows(sc[:S * k].view(S * k, 1), keep[cur], n_dev=cnt[0:1], n_max=S * k,
                         out=prev_nx.view(M0, 1), stream=stream)

@@ -89,7 +89,9 @@ def _run(kb, work, sample_per_step):
                     assert pa[s0, r] - s0 * k == par[i, r] - off[i], f"step {t} sentence {s0} rank {r}: parent"
         checked["naive"] += S
 
+    p0_in = p0.clone()
     stats = decode_loop(h_table, W, b, L, p0, k, work.T, compact=True, on_step=on_step)
+    assert torch.equal(p0, p0_in), "the loop must not write into the caller's step-0 scores"
     want_rows = [k * int((work.lengths > t).sum()) for t in range(int(work.lengths.max()))]
     assert stats.rows == want_rows
     # step t is launched sized by step t - 1's batch; a last, empty launch
@@ -97,6 +99,7 @@ def _run(kb, work, sample_per_step):
     assert stats.launch_rows[:len(want_rows)] == want_rows[:1] + want_rows[:-1]
     assert stats.launch_rows[len(want_rows):] == ([want_rows[-1]] if len(want_rows) < work.T else [])
     naive = decode_loop(h_table, W, b, L, p0, k, work.T, compact=False)
+    assert torch.equal(p0, p0_in)
     assert naive.steps == stats.steps == int(work.lengths.max())
     assert naive.total_rows == stats.total_rows
     say(f"decode: {stats.steps} steps, {stats.total_rows} live rows, checked {checked}")
