@@ -111,7 +111,8 @@ size_t kb_kbest_workspace_bytes(int dtype, int N, int H, int V, int k, int S);
  *   out_token     S x k int32: word index in [0, V).
  *   out_parent    S x k int32: global row index of the parent hypothesis.
  *   out_score     S x k float32: cumulative log-probability, descending.
- *   out_row_lse   nullable; N float32 log-sum-exp of each row.
+ *   out_row_lse   nullable; N float32 log-sum-exp of each row of a sentence
+ *                 (rows from off[S] on are not written).
  *   workspace     device scratch of at least kb_kbest_workspace_bytes(...)
  *                 bytes, 256-byte aligned; contents need no initialisation
  *                 and are overwritten.
