@@ -114,3 +114,31 @@ def test_decode_loop_config4(kb):
     work = wl.make_loop_workload()
     say(f"decode-loop workload: S={work.S} V={work.V} H={work.H} T={work.T}")
     _run(kb, work, sample_per_step=2)
+
+
+def test_decode_loop_on_its_own_stream(kb):
+    # the loop's kernels, count read-back and events all follow the stream it
+    # is given, while torch's current stream stays the default one
+    from paper_1805_09863_amd.decode import decode_loop
+    work = wl.make_loop_workload(S=40, V=3001, H=128, T=10, Lmin=1, Lmax=10, seed=77)
+    h_table, W, b, L, p0 = _upload(work)
+    want = [work.k * int((work.lengths > t).sum()) for t in range(int(work.lengths.max()))]
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for compact in (True, False):
+        got = []
+
+        def on_step(t, st):
+            with torch.cuda.stream(s):
+                got.append((st["token"].clone(), st["score"].clone()))
+        stats = decode_loop(h_table, W, b, L, p0, work.k, work.T, compact=compact, on_step=on_step, stream=s)
+        s.synchronize()
+        assert stats.rows == want
+        ref = []
+        decode_loop(h_table, W, b, L, p0, work.k, work.T, compact=compact,
+                    on_step=lambda t, st: ref.append((st["token"].clone(), st["score"].clone())))
+        torch.cuda.synchronize()
+        assert len(got) == len(ref)
+        for (ta, sa), (tb, sb) in zip(got, ref):
+            assert torch.equal(ta.cpu(), tb.cpu()) and torch.equal(sa.cpu(), sb.cpu())
+    say(f"decode loop on a side stream: {len(want)} steps, rows {want[:4]}...")
