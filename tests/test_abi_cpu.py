@@ -197,3 +197,17 @@ def test_shard_argument_checks():
     assert mp(10, 4, 5, 2, 4, *out, None, None) == KB_ERR_INVALID_ARG                            # k > V
     assert mp(2, 1000, 5, 3, 4, *out, None, None) == KB_ERR_INVALID_ARG                          # N < S
     assert mp(10, 1000, 5, 2, 4, None, *out[1:], None, None) == KB_ERR_INVALID_ARG
+
+
+def test_host_tensors_are_refused_not_computed():
+    # the product path has no host fallback: tensors off the GPU are an error
+    import torch
+    h = torch.zeros((5, 64), dtype=torch.float32)
+    W = torch.zeros((64, 100), dtype=torch.float32)
+    b = torch.zeros(100, dtype=torch.float32)
+    prev = torch.zeros(5, dtype=torch.float32)
+    off = torch.tensor([0, 5], dtype=torch.int32)
+    with pytest.raises(TypeError, match="on the GPU"):
+        kb.kbest_step(h, W, b, prev, off, 3)
+    with pytest.raises(TypeError, match="on the GPU"):
+        kb.compact_batch(torch.ones(10, dtype=torch.uint8), 2, 5)
