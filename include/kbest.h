@@ -16,8 +16,9 @@
  * ---------------------------------------
  *  - Every buffer argument is device memory owned by the caller (hipMalloc'd
  *    or a framework tensor on the current device).  The library never
- *    allocates, frees or synchronises, and keeps no mutable global state;
- *    only the text returned by kb_last_error() is per thread.
+ *    allocates, frees or synchronises (KB_DEBUG below aside), and keeps no
+ *    mutable global state; only the text returned by kb_last_error() is per
+ *    thread.
  *  - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream).
  *    Inputs must stay alive, and outputs must not be read, until the caller
  *    has synchronised with that stream.
@@ -26,6 +27,17 @@
  *    KB_ERR_HIP, which reports a failed launch.
  *  - Inputs must be finite.  Non-finite inputs give unspecified results but
  *    no fault.
+ *  - Device-resident index arrays (sentence offsets, entry sentence ids) are
+ *    trusted.  With the environment variable KB_DEBUG=1 at call time, the
+ *    calls that take them first run a validation kernel on `stream`, wait
+ *    for it (the one case in which the library synchronises) and return
+ *    KB_ERR_INVALID_ARG, with nothing else enqueued, if the contents break
+ *    the stated preconditions.  The verdict word is written into the first
+ *    int32 of an output of the call (out_token, kept_count), which the call
+ *    overwrites when it goes ahead.
+ *  - Size limits (KB_ERR_UNSUPPORTED beyond them): N * V <= INT_MAX (a
+ *    sentence's flat candidate index row * V + word is an int32), N * H
+ *    elements of h below 4 GiB, N * k and S * k within int32.
  */
 #ifndef KBEST_H
 #define KBEST_H
@@ -37,7 +49,7 @@
 extern "C" {
 #endif
 
-#define KB_ABI_VERSION 1
+#define KB_ABI_VERSION 2
 #define KB_MAX_K 16 /* largest k (beam width of the output) supported */
 
 typedef enum kb_status {
@@ -59,7 +71,7 @@ typedef enum kb_dtype {
 int kb_abi_version(void);
 
 /* Static text for a kb_status value. */
-const char* kb_status_string(int status);
+const char* kb_status_string(kb_status status);
 
 /* Detail of the last failure on the calling thread ("" if none). */
 const char* kb_last_error(void);
@@ -106,8 +118,8 @@ size_t kb_kbest_workspace_bytes(int dtype, int N, int H, int V, int k, int S);
  *                 A sentence with no rows gets k entries with token and
  *                 parent -1 and score -inf; rows from off[S] on are projected
  *                 but belong to no sentence (a step sized by an upper bound,
- *                 see kb_compact_batch).  Device contents are trusted (not
- *                 checked).
+ *                 see kb_compact_beams).  Device contents are trusted
+ *                 (checked only under KB_DEBUG=1).
  *   out_token     S x k int32: word index in [0, V).
  *   out_parent    S x k int32: global row index of the parent hypothesis.
  *   out_score     S x k float32: cumulative log-probability, descending.
@@ -120,7 +132,7 @@ size_t kb_kbest_workspace_bytes(int dtype, int N, int H, int V, int k, int S);
  * h and W must be aligned to their element size; 16-byte alignment with H
  * and V multiples of 8 (bf16) or 4 (f32) enables vector loads.
  */
-int kb_kbest_step(int dtype, int N, int H, int V, int k, int S,
+kb_status kb_kbest_step(int dtype, int N, int H, int V, int k, int S,
                   const void* h, const void* W, const float* b,
                   const float* prev_score, const int32_t* sent_offsets,
                   int32_t* out_token, int32_t* out_parent, float* out_score,
@@ -132,7 +144,7 @@ int kb_kbest_step(int dtype, int N, int H, int V, int k, int S,
  * (hipEvent_t, both nullable) on `stream` immediately before and after the
  * fused projection kernel, so a caller can time that kernel alone.
  */
-int kb_kbest_step_events(int dtype, int N, int H, int V, int k, int S,
+kb_status kb_kbest_step_events(int dtype, int N, int H, int V, int k, int S,
                          const void* h, const void* W, const float* b,
                          const float* prev_score, const int32_t* sent_offsets,
                          int32_t* out_token, int32_t* out_parent, float* out_score,
@@ -157,7 +169,7 @@ int kb_kbest_step_events(int dtype, int N, int H, int V, int k, int S,
  * words whose scores differ by less than the accumulation error may swap.
  */
 size_t kb_argmax_workspace_bytes(int dtype, int N, int H, int V);
-int kb_argmax_step(int dtype, int N, int H, int V, const void* h, const void* W, const float* b,
+kb_status kb_argmax_step(int dtype, int N, int H, int V, const void* h, const void* W, const float* b,
                    int32_t* out_token, float* out_logit, void* workspace, size_t workspace_bytes,
                    void* stream);
 
@@ -185,7 +197,7 @@ int kb_argmax_step(int dtype, int N, int H, int V, const void* h, const void* W,
  *                 Events beyond n_events or NULL entries are skipped.
  */
 size_t kb_unfused_workspace_bytes(int dtype, int N, int H, int V, int k, int S);
-int kb_kbest_step_unfused(int mode, int dtype, int N, int H, int V, int k, int S, const void* h,
+kb_status kb_kbest_step_unfused(int mode, int dtype, int N, int H, int V, int k, int S, const void* h,
                           const void* W, const float* b, const float* prev_score,
                           const int32_t* sent_offsets, int32_t* out_token, int32_t* out_parent,
                           float* out_score, float* out_row_lse, void* workspace,
@@ -197,8 +209,40 @@ int kb_kbest_step_unfused(int mode, int dtype, int N, int H, int V, int k, int S
  * Algorithm 2: after each Decode, every hypothesis that produced EOS leaves
  * the batch; decoding stops when the batch is empty).
  *
- * The batch is the S x k output of kb_kbest_step, sentence-major: entry
- * i = s*k + r is the r-th continuation of sentence s.
+ * The batch is a list of M entries (hypotheses), optionally tagged with the
+ * sentence each belongs to.
+ *   M                 entries, 0 <= M.
+ *   alive_mask        M uint8, nonzero = the entry stays in the batch.
+ *   keep_idx          M int32; the first *kept_count entries receive the
+ *                     indices of the surviving entries in ascending order (a
+ *                     stable compaction); the rest is left untouched.
+ *   kept_count        device int32 scalar: number of surviving entries.
+ *   entry_sentence    nullable, M int32: sentence id of every entry, >= 0 and
+ *                     non-decreasing along the list (entries of a sentence
+ *                     are contiguous).  Required by the two outputs below.
+ *   new_sent_offsets  nullable, receives *new_S + 1 int32: for every
+ *                     surviving sentence (one with a surviving entry), in
+ *                     order, the position of its first surviving entry in
+ *                     keep_idx, then *kept_count.  Needs room for one more
+ *                     entry than entry_sentence has distinct ids.
+ *   new_S             nullable, device int32 scalar: surviving sentences.
+ *   workspace         kb_compact_workspace_bytes(M) bytes of device scratch
+ *                     (NULL allowed when that is 0), 4-byte aligned.
+ * M == 0 writes kept_count = 0 (new_S = 0, new_sent_offsets[0] = 0).
+ * Integer work: results are exact.  KB_DEBUG=1 checks entry_sentence.
+ */
+size_t kb_compact_workspace_bytes(int M);
+kb_status kb_compact_batch(int M, const uint8_t* alive_mask, int32_t* keep_idx,
+                           int32_t* kept_count, const int32_t* entry_sentence,
+                           int32_t* new_sent_offsets, int32_t* new_S,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * kb_compact_beams -- kb_compact_batch for the S x k output of kb_kbest_step,
+ * the shape a beam decoder compacts every step (Section 2.1, Algorithm 2).
+ * Entry i = s*k + r is the r-th continuation of sentence s; the sentence ids
+ * are implicit, no workspace is needed, and the surviving sentences' old
+ * indices are reported as well.
  *   alive             S*k uint8, nonzero = the entry stays in the batch.
  *   keep_idx          S*k int32; the first *kept_count entries receive the
  *                     indices of the surviving entries in ascending order
@@ -215,25 +259,25 @@ int kb_kbest_step_unfused(int mode, int dtype, int N, int H, int V, int k, int S
  *                     index in the old batch.
  *   new_S             nullable, device int32 scalar: surviving sentences.
  * S == 0 writes kept_count = 0 (and new_S = 0, new_sent_offsets[0] = 0).
- * 1 <= k; S*k must fit in int32.  Results are exact (integer work).
+ * 1 <= k <= 1023; S*k must fit in int32.  Results are exact (integer work).
  */
-int kb_compact_batch(int S, int k, const uint8_t* alive, int32_t* keep_idx,
-                     int32_t* kept_count, int32_t* new_sent_offsets,
-                     int32_t* kept_sentence, int32_t* new_S, void* stream);
+kb_status kb_compact_beams(int S, int k, const uint8_t* alive, int32_t* keep_idx,
+                           int32_t* kept_count, int32_t* new_sent_offsets,
+                           int32_t* kept_sentence, int32_t* new_S, void* stream);
 
 /*
  * kb_beam_finish -- per-hypothesis end of sentence after a step (Section 2.1,
  * Algorithm 2: every hypothesis that produced EOS leaves the batch; the
  * sentence's beam shrinks with it, and the sentence is done when its beam is
  * empty).  Run after kb_kbest_step(k) on the same S x k outputs, then
- * kb_compact_batch on `alive`.  One step t of T (0 <= t < T):
+ * kb_compact_beams on `alive`.  One step t of T (0 <= t < T):
  *   token, parent, score   S x k outputs of kb_kbest_step (sorted per sentence).
  *   sent_id                S int32: original id (0..S0-1) of each live sentence.
  *   beam                   S int32, in/out: the sentence's beam size k_s <= k;
  *                          only its first k_s continuations are taken.  On
  *                          return, k_s minus the continuations that finished.
  *   prev_keep, prev_hist_base
- *                          the previous step's kb_compact_batch keep_idx and
+ *                          the previous step's kb_compact_beams keep_idx and
  *                          that step's hist_base: row i of this step's batch
  *                          holds the hypothesis with history id
  *                          prev_hist_base + prev_keep[i]; NULL at the first
@@ -247,11 +291,11 @@ int kb_compact_batch(int S, int k, const uint8_t* alive, int32_t* keep_idx,
  *                          included), fin_len (tokens, EOS included = t + 1),
  *                          fin_hist (history id of its last token).
  *   alive                  S*k uint8 out: 1 for taken continuations that did
- *                          not finish (the input of kb_compact_batch).
+ *                          not finish (the input of kb_compact_beams).
  * A taken continuation finishes if its token is `eos`, or at the last step
  * (t == T - 1) whatever it is.  Integer work except for copied scores: exact.
  */
-int kb_beam_finish(int S, int k, int t, int T, int eos, const int32_t* token, const int32_t* parent,
+kb_status kb_beam_finish(int S, int k, int t, int T, int eos, const int32_t* token, const int32_t* parent,
                    const float* score, const int32_t* sent_id, int32_t* beam, const int32_t* prev_keep,
                    int prev_hist_base, int hist_base, int32_t* hist_token, int32_t* hist_parent,
                    int32_t* fin_count, float* fin_score, int32_t* fin_len, int32_t* fin_hist,
@@ -266,7 +310,7 @@ int kb_beam_finish(int S, int k, int t, int T, int eos, const int32_t* token, co
  *   out_len     S0 int32 (0 for a sentence with nothing finished);
  *   out_score   S0 float32, the raw score;  out_norm  S0 float32, normalised.
  */
-int kb_beam_backtrace(int S0, int k, int T, float alpha, const int32_t* fin_count, const float* fin_score,
+kb_status kb_beam_backtrace(int S0, int k, int T, float alpha, const int32_t* fin_count, const float* fin_score,
                       const int32_t* fin_len, const int32_t* fin_hist, const int32_t* hist_token,
                       const int32_t* hist_parent, int32_t* out_tokens, int32_t* out_len, float* out_score,
                       float* out_norm, void* stream);
@@ -275,10 +319,10 @@ int kb_beam_backtrace(int S0, int k, int T, float alpha, const int32_t* fin_coun
  * kb_gather_rows -- dst[i, :] = src[idx[i], :] for i < n, where
  * n = min(n_max, *n_dev) if n_dev is non-null, else n_max.  Rows are
  * row_bytes long (a multiple of 4); src, dst 4-byte aligned.  Moves the
- * per-hypothesis state of the surviving entries after kb_compact_batch.
+ * per-hypothesis state of the surviving entries after compaction.
  * idx values must index valid rows of src (not checked).
  */
-int kb_gather_rows(int n_max, const int32_t* n_dev, const int32_t* idx,
+kb_status kb_gather_rows(int n_max, const int32_t* n_dev, const int32_t* idx,
                    const void* src, void* dst, size_t row_bytes, void* stream);
 
 /*
@@ -321,14 +365,14 @@ int kb_gather_rows(int n_max, const int32_t* n_dev, const int32_t* idx,
  *   prev_score, sent_offsets, out_* as kb_kbest_step (out_row_lse nullable).
  *   Token, parent and score follow kb_kbest_step's order and tie rule.
  */
-int kb_shard_splits(int dtype, int N, int H, int V_shard, int k, const void* h,
+kb_status kb_shard_splits(int dtype, int N, int H, int V_shard, int k, const void* h,
                     const void* W_shard, const float* b_shard, int* splits);
 size_t kb_shard_workspace_bytes(int dtype, int N, int H, int V_shard, int k);
-int kb_shard_partials(int dtype, int N, int H, int V_shard, int word_base, int k,
+kb_status kb_shard_partials(int dtype, int N, int H, int V_shard, int word_base, int k,
                       const void* h, const void* W_shard, const float* b_shard,
                       float* stats, int32_t* lists,
                       void* workspace, size_t workspace_bytes, void* stream);
-int kb_merge_partials(int N, int V, int k, int S, int P, const float* stats,
+kb_status kb_merge_partials(int N, int V, int k, int S, int P, const float* stats,
                       const int32_t* lists, const float* prev_score,
                       const int32_t* sent_offsets, int32_t* out_token,
                       int32_t* out_parent, float* out_score, float* out_row_lse,

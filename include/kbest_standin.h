@@ -29,27 +29,27 @@ extern "C" {
  * loop that sizes a step by an upper bound S on the sentence count passes the
  * exact count on the device, and the entries of sentences past it are 0 (sid
  * is not read for them).
- *   S_dev    NULL or one int32 on the device (e.g. kb_compact_batch's new_S).
+ *   S_dev    NULL or one int32 on the device (e.g. kb_compact_beams's new_S).
  *   sid      S int32, original sentence ids (indices into lengths).
  *   lengths  int32 per original sentence.
- *   alive    S*k uint8 output, the input of kb_compact_batch.
+ *   alive    S*k uint8 output, the input of kb_compact_beams.
  * S == 0 is a no-op.  0 <= S, 1 <= k, S*k fits in int32.
  */
-int kb_standin_alive(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
+kb_status kb_standin_alive(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
                      uint8_t* alive, void* stream);
 
 /*
  * kb_standin_next_h -- the states of step t for the entries kept by
- * kb_compact_batch: for i < n = min(n_max, *n_dev) (n_max if n_dev is NULL),
+ * kb_compact_beams: for i < n = min(n_max, *n_dev) (n_max if n_dev is NULL),
  *   e = keep[i];  out[i, :] = table[(sid[e / k] * T + t) * k + e % k, :]
  * i.e. the table row of (original sentence sid[e / k], step t, beam slot
  * e % k); rows are row_bytes long (a positive multiple of 4).
- *   keep     kb_compact_batch's keep_idx (entries of the old S x k batch).
+ *   keep     kb_compact_beams's keep_idx (entries of the old S x k batch).
  *   sid      the OLD batch's original sentence ids (S_old int32).
  *   table    (S0 * T * k) rows; out at least n_max rows.  4-byte aligned.
  * 0 <= t < T; keep and sid must index valid entries (not checked).
  */
-int kb_standin_next_h(int n_max, const int32_t* n_dev, int k, int T, int t, const int32_t* keep,
+kb_status kb_standin_next_h(int n_max, const int32_t* n_dev, int k, int T, int t, const int32_t* keep,
                       const int32_t* sid, const void* table, void* out, size_t row_bytes, void* stream);
 
 #ifdef __cplusplus

@@ -140,7 +140,7 @@ def kbest_step(h, W, b, prev, off, k: int, dtype: str = "f32") -> KBestResult:
 
 
 def kbest_step_threshold(h, W, b, prev, off, k: int, dtype: str = "f32",
-                         sentences=None) -> KBestResult:
+                         sentences=None, row_block: int = 256) -> KBestResult:
     """Same result as :func:`kbest_step`, with an exact shortcut for large inputs.
 
     Per sentence: tau = the (k+1)-th largest score (``np.partition``); every
@@ -151,7 +151,8 @@ def kbest_step_threshold(h, W, b, prev, off, k: int, dtype: str = "f32",
 
     ``sentences`` restricts the work (and the returned rows of token /
     parent / score / next_score) to the listed sentences; ``lse`` is then
-    filled only on their rows (NaN elsewhere).
+    filled only on their rows (NaN elsewhere).  ``row_block`` bounds the rows
+    whose logits are held at once (whole sentences; memory only).
     """
     W64 = widen(W, dtype)
     b64 = np.asarray(b, dtype=np.float32).astype(np.float64)
@@ -165,24 +166,39 @@ def kbest_step_threshold(h, W, b, prev, off, k: int, dtype: str = "f32",
     sc = np.zeros((len(sel), k), dtype=np.float64)
     nxt = np.full(len(sel), -np.inf)
     lse_all = np.full(N, np.nan)
-    for i, s in enumerate(sel):
-        r0, r1 = off[s], off[s + 1]
-        x = logits(widen(h[r0:r1], dtype), W64, b64)
-        logp, lse = log_softmax(x)
-        lse_all[r0:r1] = lse
-        f = (prev32[r0:r1].astype(np.float64)[:, None] + logp).reshape(-1)
-        if f.size > k:
-            tau = np.partition(f, f.size - (k + 1))[f.size - (k + 1)]
-            idx = np.flatnonzero(f >= tau)
-        else:
-            idx = np.arange(f.size)
-        order = idx[np.argsort(-f[idx], kind="stable")]
-        top = order[:k]
-        tok[i] = top % V
-        par[i] = r0 + top // V
-        sc[i] = f[top]
-        if order.size > k:
-            nxt[i] = f[order[k]]
+    # the logits of several sentences' rows come from one product (each row's
+    # value is the same sum h[n] . W[:, j] + b[j]); then each sentence is
+    # ranked on its own
+    i = 0
+    while i < len(sel):
+        j, nrows = i, 0
+        while j < len(sel) and (j == i or nrows + off[sel[j] + 1] - off[sel[j]] <= row_block):
+            nrows += off[sel[j] + 1] - off[sel[j]]
+            j += 1
+        rows = np.concatenate([np.arange(off[s], off[s + 1]) for s in sel[i:j]]).astype(np.int64)
+        xb = logits(widen(h[rows], dtype), W64, b64)
+        pos = 0
+        for q in range(i, j):
+            s = sel[q]
+            r0, r1 = off[s], off[s + 1]
+            x = xb[pos:pos + (r1 - r0)]
+            pos += r1 - r0
+            logp, lse = log_softmax(x)
+            lse_all[r0:r1] = lse
+            f = (prev32[r0:r1].astype(np.float64)[:, None] + logp).reshape(-1)
+            if f.size > k:
+                tau = np.partition(f, f.size - (k + 1))[f.size - (k + 1)]
+                idx = np.flatnonzero(f >= tau)
+            else:
+                idx = np.arange(f.size)
+            order = idx[np.argsort(-f[idx], kind="stable")]
+            top = order[:k]
+            tok[q] = top % V
+            par[q] = r0 + top // V
+            sc[q] = f[top]
+            if order.size > k:
+                nxt[q] = f[order[k]]
+        i = j
     return KBestResult(tok, par, sc, nxt, lse_all)
 
 
@@ -343,3 +359,23 @@ def compact(alive, S: int, k: int) -> CompactResult:
     ks = np.flatnonzero(per_sent > 0)
     new_off = np.concatenate([[0], np.cumsum(per_sent[ks])]).astype(np.int64)
     return CompactResult(keep, int(keep.size), new_off, ks, int(ks.size))
+
+
+def compact_entries(alive, entry_sentence=None) -> CompactResult:
+    """Section 2.1, Algorithm 2 on a batch given as a flat list of M entries.
+
+    Every entry whose ``alive`` flag is 0 (its hypothesis produced EOS) leaves
+    the batch; the rest keep their order (``keep_idx``).  With the sentence id
+    of every entry (non-decreasing along the list), a sentence stays in the
+    batch if any of its entries does; its new offset counts the surviving
+    entries of the sentences before it.  ``kept_sentence`` holds the ids of the
+    surviving sentences.
+    """
+    a = np.asarray(alive).reshape(-1).astype(bool)
+    keep = np.flatnonzero(a)
+    if entry_sentence is None:
+        return CompactResult(keep, int(keep.size), np.zeros(0, np.int64), np.zeros(0, np.int64), 0)
+    es = np.asarray(entry_sentence).reshape(-1).astype(np.int64)
+    ks, per_sent = np.unique(es[keep], return_counts=True)   # sorted ids with a surviving entry
+    new_off = np.concatenate([[0], np.cumsum(per_sent)]).astype(np.int64)
+    return CompactResult(keep, int(keep.size), new_off, ks.astype(np.int64), int(ks.size))

@@ -7,6 +7,6 @@ work runs in the HIP kernels of ``libkbest.so`` (C ABI in include/kbest.h);
 this package only marshals arguments to it.
 """
 from .binding import (KB_BF16, KB_F32, KB_MAX_K, KBestError, abi_version, argmax_step,  # noqa: F401
-                      argmax_workspace_bytes, compact_batch, gather_rows, kbest_step, kbest_step_unfused,
+                      argmax_workspace_bytes, compact_batch, compact_beams, compact_workspace_bytes, gather_rows, kbest_step, kbest_step_unfused,
                       kbest_workspace_bytes, lib, merge_partials, shard_partials, shard_splits,
                       unfused_workspace_bytes, workspace)

@@ -41,7 +41,9 @@ SIGNATURES = {
                                    _P, _I, _P]),
     "kb_beam_finish": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P]),
     "kb_beam_backtrace": (_I, [_I, _I, _I, ctypes.c_float, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
-    "kb_compact_batch": (_I, [_I, _I, _P, _P, _P, _P, _P, _P, _P]),
+    "kb_compact_workspace_bytes": (_SZ, [_I]),
+    "kb_compact_batch": (_I, [_I, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "kb_compact_beams": (_I, [_I, _I, _P, _P, _P, _P, _P, _P, _P]),
     "kb_gather_rows": (_I, [_I, _P, _P, _P, _P, _SZ, _P]),
     "kb_shard_splits": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _P]),
     "kb_shard_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I]),
@@ -98,7 +100,9 @@ def _dtype_code(t: torch.Tensor) -> int:
     raise TypeError(f"h and W must be float32 or bfloat16, got {t.dtype}")
 
 
-def _need(t: torch.Tensor, name: str, dtype=None, dim=None):
+def _need(t: torch.Tensor, name: str, dtype=None, dim=None, numel=None):
+    """Every tensor handed to the library as a pointer: on the GPU, contiguous,
+    of the given type and rank, and (numel) at least that many elements."""
     if not isinstance(t, torch.Tensor) or not t.is_cuda:
         raise TypeError(f"{name} must be a tensor on the GPU")
     if not t.is_contiguous():
@@ -107,6 +111,21 @@ def _need(t: torch.Tensor, name: str, dtype=None, dim=None):
         raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
     if dim is not None and t.dim() != dim:
         raise ValueError(f"{name} must have {dim} dimensions")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name} has {t.numel()} elements, {numel} needed")
+
+
+def _need_ws(ws: torch.Tensor, nbytes: int, name: str = "ws"):
+    _need(ws, name)
+    if ws.numel() * ws.element_size() < nbytes:
+        raise ValueError(f"{name} has {ws.numel() * ws.element_size()} bytes, {nbytes} needed")
+
+
+def _need_outs(out, names, dtypes, numel):
+    if len(out) != len(names):
+        raise ValueError(f"out must hold {len(names)} tensors ({', '.join(names)})")
+    for t, n, d in zip(out, names, dtypes):
+        _need(t, n, dtype=d, numel=numel)
 
 
 def abi_version() -> int:
@@ -154,12 +173,14 @@ def kbest_step(h: torch.Tensor, W: torch.Tensor, b: torch.Tensor, prev_score: to
         par = torch.empty((S, k), dtype=torch.int32, device=dev)
         sc = torch.empty((S, k), dtype=torch.float32, device=dev)
     else:
+        _need_outs(out, ("token", "parent", "score"), (torch.int32, torch.int32, torch.float32), S * k)
         tok, par, sc = out
     need = kbest_workspace_bytes(dt, N, H, V, k, S)
     if ws is None:
         ws = workspace(need, dev)
+    _need_ws(ws, need)
     if row_lse is not None:
-        _need(row_lse, "row_lse", dtype=torch.float32, dim=1)
+        _need(row_lse, "row_lse", dtype=torch.float32, numel=N)
     L = lib()
     args = [dt, N, H, V, k, S, _ptr(h), _ptr(W), _ptr(b), _ptr(prev_score), _ptr(sent_offsets),
             _ptr(tok), _ptr(par), _ptr(sc), _ptr(row_lse), _ptr(ws), ws.numel() * ws.element_size(),
@@ -191,9 +212,12 @@ def argmax_step(h: torch.Tensor, W: torch.Tensor, b: torch.Tensor, *, out: Optio
         tok = torch.empty(N, dtype=torch.int32, device=h.device)
         val = torch.empty(N, dtype=torch.float32, device=h.device)
     else:
+        _need_outs(out, ("token", "logit"), (torch.int32, torch.float32), N)
         tok, val = out
+    need = argmax_workspace_bytes(dt, N, H, V)
     if ws is None:
-        ws = workspace(argmax_workspace_bytes(dt, N, H, V), h.device)
+        ws = workspace(need, h.device)
+    _need_ws(ws, need)
     _check(lib().kb_argmax_step(dt, N, H, V, _ptr(h), _ptr(W), _ptr(b), _ptr(tok), _ptr(val), _ptr(ws),
                                 ws.numel() * ws.element_size(), _stream(stream)))
     return tok, val
@@ -222,9 +246,14 @@ def kbest_step_unfused(h: torch.Tensor, W: torch.Tensor, b: torch.Tensor, prev_s
     if out is None:
         out = tuple(torch.empty((S, k), dtype=t, device=h.device)
                     for t in (torch.int32, torch.int32, torch.float32))
+    _need_outs(out, ("token", "parent", "score"), (torch.int32, torch.int32, torch.float32), S * k)
     tok, par, sc = out
+    need = unfused_workspace_bytes(dt, N, H, V, k, S)
     if ws is None:
-        ws = workspace(unfused_workspace_bytes(dt, N, H, V, k, S), h.device)
+        ws = workspace(need, h.device)
+    _need_ws(ws, need)
+    if row_lse is not None:
+        _need(row_lse, "row_lse", dtype=torch.float32, numel=N)
     ev = None
     if events:
         ev = (ctypes.c_void_p * len(events))(*[ctypes.c_void_p(e) for e in events])
@@ -235,8 +264,53 @@ def kbest_step_unfused(h: torch.Tensor, W: torch.Tensor, b: torch.Tensor, prev_s
     return tok, par, sc
 
 
-def compact_batch(alive: torch.Tensor, S: int, k: int, *, out: Optional[tuple] = None, stream=None):
-    """Stable removal of finished entries (Algorithm 2).
+def compact_workspace_bytes(M: int) -> int:
+    return int(lib().kb_compact_workspace_bytes(M))
+
+
+def compact_batch(alive: torch.Tensor, entry_sentence: Optional[torch.Tensor] = None, *,
+                  out: Optional[tuple] = None, ws: Optional[torch.Tensor] = None, stream=None):
+    """Stable removal of finished entries from a batch of M entries (Algorithm 2).
+
+    ``alive`` is M uint8 on the GPU; ``entry_sentence`` (optional) M int32,
+    the non-decreasing sentence id of every entry.  Returns device tensors
+    (keep_idx[M], kept_count[1], new_sent_offsets, new_S[1]); only the first
+    kept_count / new_S + 1 entries are meaningful.  Without entry_sentence the
+    last two are None.  ``out`` may supply (keep_idx, kept_count,
+    new_sent_offsets, new_S); new_sent_offsets needs one more entry than
+    entry_sentence has distinct ids (M + 1 always suffices).
+    """
+    _need(alive, "alive", dtype=torch.uint8, dim=1)
+    M = alive.numel()
+    dev = alive.device
+    if entry_sentence is not None:
+        _need(entry_sentence, "entry_sentence", dtype=torch.int32, dim=1, numel=M)
+    if out is None:
+        keep = torch.empty(max(M, 1), dtype=torch.int32, device=dev)
+        kept = torch.empty(1, dtype=torch.int32, device=dev)
+        noff = torch.empty(M + 1, dtype=torch.int32, device=dev) if entry_sentence is not None else None
+        nS = torch.empty(1, dtype=torch.int32, device=dev) if entry_sentence is not None else None
+    else:
+        keep, kept, noff, nS = out
+        _need(keep, "keep_idx", dtype=torch.int32, numel=M)
+        _need(kept, "kept_count", dtype=torch.int32, numel=1)
+        if noff is not None:
+            _need(noff, "new_sent_offsets", dtype=torch.int32, numel=1)
+        if nS is not None:
+            _need(nS, "new_S", dtype=torch.int32, numel=1)
+    need = compact_workspace_bytes(M)
+    if ws is None and need > 0:
+        ws = workspace(need, dev)
+    if ws is not None:
+        _need_ws(ws, need)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().kb_compact_batch(M, _ptr(alive), _ptr(keep), _ptr(kept), _ptr(entry_sentence), _ptr(noff),
+                                  _ptr(nS), _ptr(ws), nbytes, _stream(stream)))
+    return keep, kept, noff, nS
+
+
+def compact_beams(alive: torch.Tensor, S: int, k: int, *, out: Optional[tuple] = None, stream=None):
+    """Stable removal of finished entries from the S x k output of a step (Algorithm 2).
 
     ``alive`` is S*k uint8 on the GPU.  Returns device tensors
     (keep_idx[S*k], kept_count[1], new_sent_offsets[S+1], kept_sentence[S], new_S[1]);
@@ -254,7 +328,15 @@ def compact_batch(alive: torch.Tensor, S: int, k: int, *, out: Optional[tuple] =
         nS = torch.empty(1, dtype=torch.int32, device=dev)
     else:
         keep, kept, noff, ksent, nS = out
-    _check(lib().kb_compact_batch(S, k, _ptr(alive), _ptr(keep), _ptr(kept), _ptr(noff), _ptr(ksent),
+        _need(keep, "keep_idx", dtype=torch.int32, numel=S * k)
+        _need(kept, "kept_count", dtype=torch.int32, numel=1)
+        if noff is not None:
+            _need(noff, "new_sent_offsets", dtype=torch.int32, numel=S + 1)
+        if ksent is not None:
+            _need(ksent, "kept_sentence", dtype=torch.int32, numel=S)
+        if nS is not None:
+            _need(nS, "new_S", dtype=torch.int32, numel=1)
+    _check(lib().kb_compact_beams(S, k, _ptr(alive), _ptr(keep), _ptr(kept), _ptr(noff), _ptr(ksent),
                                   _ptr(nS), _stream(stream)))
     return keep, kept, noff, ksent, nS
 
@@ -263,11 +345,14 @@ def gather_rows(src: torch.Tensor, idx: torch.Tensor, *, n_dev: Optional[torch.T
                 n_max: Optional[int] = None, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """out[i] = src[idx[i]] for i < min(n_max, n_dev[0]) (rows of src along dim 0)."""
     _need(src, "src")
-    _need(idx, "idx", dtype=torch.int32, dim=1)
     n_max = idx.shape[0] if n_max is None else n_max
+    _need(idx, "idx", dtype=torch.int32, dim=1, numel=n_max)
+    if n_dev is not None:
+        _need(n_dev, "n_dev", dtype=torch.int32, numel=1)
     row_bytes = src[0].numel() * src.element_size() if src.shape[0] > 0 else 0
     if out is None:
         out = torch.empty((n_max,) + tuple(src.shape[1:]), dtype=src.dtype, device=src.device)
+    _need(out, "out", dtype=src.dtype, numel=n_max * (src[0].numel() if src.shape[0] > 0 else 0))
     if n_max == 0:
         return out
     _check(lib().kb_gather_rows(n_max, _ptr(n_dev), _ptr(idx), _ptr(src), _ptr(out), row_bytes,
@@ -304,8 +389,10 @@ def shard_partials(h: torch.Tensor, W_shard: torch.Tensor, b_shard: torch.Tensor
     if stats.numel() < P * N * 2 or lists.numel() < P * N * k * 2:
         raise ValueError(f"stats / lists too small for {P} splits")
     dt = _dtype_code(h)
+    need = int(lib().kb_shard_workspace_bytes(dt, N, H, V_shard, k))
     if ws is None:
-        ws = workspace(lib().kb_shard_workspace_bytes(dt, N, H, V_shard, k), h.device)
+        ws = workspace(need, h.device)
+    _need_ws(ws, need)
     _check(lib().kb_shard_partials(dt, N, H, V_shard, word_base, k, _ptr(h), _ptr(W_shard), _ptr(b_shard),
                                    _ptr(stats), _ptr(lists), _ptr(ws), ws.numel() * ws.element_size(),
                                    _stream(stream)))
@@ -328,7 +415,10 @@ def merge_partials(stats: torch.Tensor, lists: torch.Tensor, P: int, V: int, k: 
     if out is None:
         out = tuple(torch.empty((S, k), dtype=t, device=prev_score.device)
                     for t in (torch.int32, torch.int32, torch.float32))
+    _need_outs(out, ("token", "parent", "score"), (torch.int32, torch.int32, torch.float32), S * k)
     tok, par, sc = out
+    if row_lse is not None:
+        _need(row_lse, "row_lse", dtype=torch.float32, numel=N)
     _check(lib().kb_merge_partials(N, V, k, S, P, _ptr(stats), _ptr(lists), _ptr(prev_score), _ptr(sent_offsets),
                                    _ptr(tok), _ptr(par), _ptr(sc), _ptr(row_lse), _stream(stream)))
     return tok, par, sc
@@ -338,6 +428,11 @@ def standin_alive(sid: torch.Tensor, lengths: torch.Tensor, S: int, k: int, t: i
                   S_dev: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """out[s*k + r] = (s < min(S, S_dev[0]) and t < lengths[sid[s]] - 1) for s < S
     (include/kbest_standin.h)."""
+    _need(sid, "sid", dtype=torch.int32, numel=S)
+    _need(lengths, "lengths", dtype=torch.int32)
+    _need(out, "out", dtype=torch.uint8, numel=S * k)
+    if S_dev is not None:
+        _need(S_dev, "S_dev", dtype=torch.int32, numel=1)
     _check(lib().kb_standin_alive(S, _ptr(S_dev), k, t, _ptr(sid), _ptr(lengths), _ptr(out), _stream(stream)))
     return out
 
@@ -345,6 +440,12 @@ def standin_alive(sid: torch.Tensor, lengths: torch.Tensor, S: int, k: int, t: i
 def standin_next_h(table: torch.Tensor, keep: torch.Tensor, sid: torch.Tensor, k: int, T: int, t: int,
                    n_max: int, *, n_dev: Optional[torch.Tensor] = None, out: torch.Tensor, stream=None):
     """out[i] = table[(sid[keep[i] // k] * T + t) * k + keep[i] % k] for i < min(n_max, n_dev[0])."""
+    _need(table, "table")
+    _need(keep, "keep", dtype=torch.int32, numel=n_max)
+    _need(sid, "sid", dtype=torch.int32)
+    _need(out, "out", dtype=table.dtype, numel=n_max * table[0].numel())
+    if n_dev is not None:
+        _need(n_dev, "n_dev", dtype=torch.int32, numel=1)
     row_bytes = table[0].numel() * table.element_size()
     _check(lib().kb_standin_next_h(n_max, _ptr(n_dev), k, T, t, _ptr(keep), _ptr(sid), _ptr(table), _ptr(out),
                                    row_bytes, _stream(stream)))
@@ -358,6 +459,18 @@ def beam_finish(S: int, k: int, t: int, T: int, eos: int, token, parent, score, 
     history, move EOS (or last-step) continuations to the finished store ``fin`` =
     (count, score, len, hist), shrink the beams and fill ``alive`` (include/kbest.h)."""
     fc, fs, fl, fh = fin
+    n = S * k
+    for t, nm, d, m in ((token, "token", torch.int32, n), (parent, "parent", torch.int32, n),
+                        (score, "score", torch.float32, n), (sent_id, "sent_id", torch.int32, S),
+                        (beam, "beam", torch.int32, S), (hist_token, "hist_token", torch.int32, hist_base + n),
+                        (hist_parent, "hist_parent", torch.int32, hist_base + n),
+                        (fc, "fin_count", torch.int32, S), (alive, "alive", torch.uint8, n)):
+        _need(t, nm, dtype=d, numel=m)
+    S0 = fc.numel()             # the finished store holds k slots per original sentence
+    for t, nm, d in ((fs, "fin_score", torch.float32), (fl, "fin_len", torch.int32), (fh, "fin_hist", torch.int32)):
+        _need(t, nm, dtype=d, numel=S0 * k)
+    if prev_keep is not None:
+        _need(prev_keep, "prev_keep", dtype=torch.int32, numel=S)
     _check(lib().kb_beam_finish(S, k, t, T, eos, _ptr(token), _ptr(parent), _ptr(score), _ptr(sent_id), _ptr(beam),
                                 _ptr(prev_keep), prev_hist_base, hist_base, _ptr(hist_token), _ptr(hist_parent),
                                 _ptr(fc), _ptr(fs), _ptr(fl), _ptr(fh), _ptr(alive), _stream(stream)))
@@ -372,6 +485,13 @@ def beam_backtrace(S0: int, k: int, T: int, alpha: float, fin: tuple, hist_token
     if out is None:
         out = (torch.empty((S0, T), dtype=torch.int32, device=dev), torch.empty(S0, dtype=torch.int32, device=dev),
                torch.empty(S0, dtype=torch.float32, device=dev), torch.empty(S0, dtype=torch.float32, device=dev))
+    for t, nm_, d in ((fc, "fin_count", torch.int32), (fs, "fin_score", torch.float32),
+                      (fl, "fin_len", torch.int32), (fh, "fin_hist", torch.int32)):
+        _need(t, nm_, dtype=d, numel=S0 * (1 if nm_ == "fin_count" else k))
+    _need(hist_token, "hist_token", dtype=torch.int32)
+    _need(hist_parent, "hist_parent", dtype=torch.int32)
+    _need_outs(out[:1], ("tokens",), (torch.int32,), S0 * T)
+    _need_outs(out[1:], ("len", "score", "norm"), (torch.int32, torch.float32, torch.float32), S0)
     toks, ln, sc, nm = out
     _check(lib().kb_beam_backtrace(S0, k, T, float(alpha), _ptr(fc), _ptr(fs), _ptr(fl), _ptr(fh), _ptr(hist_token),
                                    _ptr(hist_parent), _ptr(toks), _ptr(ln), _ptr(sc), _ptr(nm), _stream(stream)))

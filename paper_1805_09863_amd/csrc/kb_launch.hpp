@@ -29,6 +29,16 @@ hipError_t launch_k2_argmax(const int2* lists, int P, int N, int32_t* tok, float
 hipError_t launch_compact(int S, int k, const uint8_t* alive, int32_t* keep, int32_t* kept_count,
                           int32_t* new_off, int32_t* kept_sent, int32_t* new_S, hipStream_t st);
 
+// M-entry form (sentence ids per entry); one workgroup up to KE_ONE entries,
+// else three kernels per pass over a workspace of compact_entries_ws_bytes(M)
+constexpr int KE_ONE = 16384;
+size_t compact_entries_ws_bytes(int M);
+hipError_t launch_compact_entries(int M, const uint8_t* alive, int32_t* keep, int32_t* kept_count, const int32_t* es,
+                                  int32_t* new_off, int32_t* new_S, void* ws, hipStream_t st);
+// KB_DEBUG validation of device-resident index arrays (flag word 0 = valid)
+hipError_t launch_check_offsets(int S, int N, const int32_t* off, int32_t* flag, hipStream_t st);
+hipError_t launch_check_sorted(int M, const int32_t* es, int32_t* flag, hipStream_t st);
+
 hipError_t launch_gather(int n_max, const int32_t* n_dev, const int32_t* idx, const void* src,
                          void* dst, size_t row_bytes, hipStream_t st);
 

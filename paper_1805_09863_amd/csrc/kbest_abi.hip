@@ -2,6 +2,7 @@
 // layout and the C entry points declared in include/kbest.h.
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <string>
@@ -62,8 +63,8 @@ namespace {
 
 thread_local std::string g_last_error;
 
-int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
-int fail(int status, const char* fmt, ...) {
+kb_status fail(kb_status status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+kb_status fail(kb_status status, const char* fmt, ...) {
   char buf[512];
   va_list ap;
   va_start(ap, fmt);
@@ -73,7 +74,7 @@ int fail(int status, const char* fmt, ...) {
   return status;
 }
 
-int ok() {
+kb_status ok() {
   g_last_error.clear();
   return KB_OK;
 }
@@ -161,7 +162,7 @@ size_t workspace_bytes(int dtype, int N, int H, int V, int k) {
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-int validate_step(int dtype, int N, int H, int V, int k, int S) {
+kb_status validate_step(int dtype, int N, int H, int V, int k, int S) {
   if (dtype != KB_F32 && dtype != KB_BF16) return fail(KB_ERR_INVALID_ARG, "unknown dtype %d", dtype);
   if (N < 0 || S < 0) return fail(KB_ERR_INVALID_ARG, "negative N (%d) or S (%d)", N, S);
   if ((N == 0) != (S == 0)) return fail(KB_ERR_INVALID_ARG, "N = %d and S = %d: both or neither must be 0", N, S);
@@ -171,8 +172,35 @@ int validate_step(int dtype, int N, int H, int V, int k, int S) {
   if (N < S) return fail(KB_ERR_INVALID_ARG, "N = %d < S = %d: N >= S is required", N, S);
   if ((long long)N * k > INT_MAX || (long long)S * k > INT_MAX || (long long)H * V > (1LL << 40))
     return fail(KB_ERR_UNSUPPORTED, "shape too large");
-  if ((long long)N * V > (1LL << 46)) return fail(KB_ERR_UNSUPPORTED, "N * V too large");
+  // a sentence's flat candidate index (row - first row) * V + word is an int32
+  if ((long long)N * V > INT_MAX) return fail(KB_ERR_UNSUPPORTED, "N * V = %lld exceeds INT_MAX", (long long)N * V);
+  // byte offsets into h are 32-bit in the projection kernels
+  if ((long long)N * H * (dtype == KB_BF16 ? 2 : 4) >= (1LL << 32)) return fail(KB_ERR_UNSUPPORTED, "h is 4 GiB or larger");
   return KB_OK;
+}
+
+// KB_DEBUG=1: validate device-resident index arrays before anything else is
+// enqueued.  The verdict word goes to `flag` (an int32 of the call's output
+// that the call overwrites when it goes ahead) and is read back after a wait.
+bool debug_checks() {
+  const char* e = getenv("KB_DEBUG");
+  return e != nullptr && e[0] == '1' && e[1] == 0;
+}
+
+kb_status debug_verdict(hipError_t e, const int32_t* flag, hipStream_t hs, const char* what) {
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "KB_DEBUG check launch: %s", hipGetErrorString(e));
+  int32_t v = -1;
+  e = hipMemcpyAsync(&v, flag, sizeof v, hipMemcpyDeviceToHost, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "KB_DEBUG check read-back: %s", hipGetErrorString(e));
+  if (v != 0) return fail(KB_ERR_INVALID_ARG, "KB_DEBUG: %s (check word 0x%x)", what, (unsigned)v);
+  return KB_OK;
+}
+
+kb_status debug_offsets(int S, int N, const int32_t* off, int32_t* flag, hipStream_t hs) {
+  if (!debug_checks()) return KB_OK;
+  return debug_verdict(kb::launch_check_offsets(S, N, off, flag, hs), flag, hs,
+                       "sent_offsets break 0 = off[0] <= off[1] <= ... <= off[S] <= N");
 }
 
 // Whether the operands allow 16-byte vector loads, and the plan they select.
@@ -189,7 +217,7 @@ Plan plan_for(int dtype, int N, int H, int V, int k, const void* h, const void* 
 // shared by the k-best step, the greedy argmax and the vocabulary shards.  On
 // KB_OK, a1 and p describe the launched projection; its partials are in the
 // workspace, or in stats_out / lists_out when given (split rows N apart).
-int launch_projection(int dtype, int N, int H, int V, int k, const void* h, const void* W, const float* b,
+kb_status launch_projection(int dtype, int N, int H, int V, int k, const void* h, const void* W, const float* b,
                       void* ws, size_t ws_bytes, hipStream_t hs, bool no_stats, void* ev0, void* ev1,
                       kb::K1Args& a1, Plan& p, float2* stats_out = nullptr, int2* lists_out = nullptr) {
   const size_t esz = dtype == KB_BF16 ? 2 : 4;
@@ -240,16 +268,17 @@ int launch_projection(int dtype, int N, int H, int V, int k, const void* h, cons
   return KB_OK;
 }
 
-int kbest_step_impl(int dtype, int N, int H, int V, int k, int S, const void* h, const void* W, const float* b,
+kb_status kbest_step_impl(int dtype, int N, int H, int V, int k, int S, const void* h, const void* W, const float* b,
                     const float* prev, const int32_t* off, int32_t* tok, int32_t* par, float* score,
                     float* row_lse, void* ws, size_t ws_bytes, void* stream, void* ev0, void* ev1) {
-  int st = validate_step(dtype, N, H, V, k, S);
+  kb_status st = validate_step(dtype, N, H, V, k, S);
   if (st != KB_OK) return st;
   if (N == 0) return ok();
   if (!h || !W || !b || !prev || !off || !tok || !par || !score)
     return fail(KB_ERR_INVALID_ARG, "null input or output pointer");
   if (!aligned(prev, 4)) return fail(KB_ERR_INVALID_ARG, "prev misaligned");
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  if ((st = debug_offsets(S, N, off, tok, hs)) != KB_OK) return st;
   kb::K1Args a1;
   Plan p;
   st = launch_projection(dtype, N, H, V, k, h, W, b, ws, ws_bytes, hs, false, ev0, ev1, a1, p);
@@ -313,7 +342,7 @@ UfPlan uf_plan(int N, int H, int V, int k) {
   return u;
 }
 
-int record(void* const* ev, int n_ev, int i, hipStream_t hs) {
+kb_status record(void* const* ev, int n_ev, int i, hipStream_t hs) {
   if (!ev || i >= n_ev || !ev[i]) return KB_OK;
   hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev[i]), hs);
   return e == hipSuccess ? KB_OK : fail(KB_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
@@ -324,7 +353,7 @@ extern "C" {
 
 int kb_abi_version(void) { return KB_ABI_VERSION; }
 
-const char* kb_status_string(int s) {
+const char* kb_status_string(kb_status s) {
   switch (s) {
     case KB_OK: return "ok";
     case KB_ERR_INVALID_ARG: return "invalid argument";
@@ -342,14 +371,14 @@ size_t kb_kbest_workspace_bytes(int dtype, int N, int H, int V, int k, int S) {
   return workspace_bytes(dtype, N, H, V, k);
 }
 
-int kb_kbest_step(int dtype, int N, int H, int V, int k, int S, const void* h, const void* W, const float* b,
+kb_status kb_kbest_step(int dtype, int N, int H, int V, int k, int S, const void* h, const void* W, const float* b,
                   const float* prev_score, const int32_t* sent_offsets, int32_t* out_token, int32_t* out_parent,
                   float* out_score, float* out_row_lse, void* workspace, size_t workspace_bytes, void* stream) {
   return kbest_step_impl(dtype, N, H, V, k, S, h, W, b, prev_score, sent_offsets, out_token, out_parent,
                          out_score, out_row_lse, workspace, workspace_bytes, stream, nullptr, nullptr);
 }
 
-int kb_kbest_step_events(int dtype, int N, int H, int V, int k, int S, const void* h, const void* W,
+kb_status kb_kbest_step_events(int dtype, int N, int H, int V, int k, int S, const void* h, const void* W,
                          const float* b, const float* prev_score, const int32_t* sent_offsets, int32_t* out_token,
                          int32_t* out_parent, float* out_score, float* out_row_lse, void* workspace,
                          size_t workspace_bytes, void* stream, void* proj_begin_event, void* proj_end_event) {
@@ -364,12 +393,12 @@ size_t kb_unfused_workspace_bytes(int dtype, int N, int H, int V, int k, int S) 
   return uf_plan(N, H, V, k).bytes;
 }
 
-int kb_kbest_step_unfused(int mode, int dtype, int N, int H, int V, int k, int S, const void* h, const void* W,
+kb_status kb_kbest_step_unfused(int mode, int dtype, int N, int H, int V, int k, int S, const void* h, const void* W,
                           const float* b, const float* prev_score, const int32_t* sent_offsets, int32_t* out_token,
                           int32_t* out_parent, float* out_score, float* out_row_lse, void* workspace,
                           size_t workspace_bytes, void* const* stage_events, int n_events, void* stream) {
   if (mode != 0 && mode != 1) return fail(KB_ERR_INVALID_ARG, "mode %d: 0 (Algorithm 3) or 1 (Algorithm 4)", mode);
-  int st = validate_step(dtype, N, H, V, k, S);
+  kb_status st = validate_step(dtype, N, H, V, k, S);
   if (st != KB_OK) return st;
   if (N == 0) return ok();
   if (!uf_shape(dtype, H, V))
@@ -383,6 +412,7 @@ int kb_kbest_step_unfused(int mode, int dtype, int N, int H, int V, int k, int S
   if (!aligned(workspace, 256)) return fail(KB_ERR_WORKSPACE, "workspace must be 256-byte aligned");
   if (workspace_bytes < u.bytes) return fail(KB_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, u.bytes);
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  if ((st = debug_offsets(S, N, sent_offsets, out_token, hs)) != KB_OK) return st;
   char* ws = static_cast<char*>(workspace);
   float* x = reinterpret_cast<float*>(ws + u.logits_off);
   float2* stats = reinterpret_cast<float2*>(ws + u.stats_off);
@@ -439,9 +469,9 @@ size_t kb_argmax_workspace_bytes(int dtype, int N, int H, int V) {
   return workspace_bytes(dtype, N, H, V, 1);
 }
 
-int kb_argmax_step(int dtype, int N, int H, int V, const void* h, const void* W, const float* b, int32_t* out_token,
+kb_status kb_argmax_step(int dtype, int N, int H, int V, const void* h, const void* W, const float* b, int32_t* out_token,
                    float* out_logit, void* workspace, size_t workspace_bytes, void* stream) {
-  int st = validate_step(dtype, N, H, V, 1, N > 0 ? 1 : 0);
+  kb_status st = validate_step(dtype, N, H, V, 1, N > 0 ? 1 : 0);
   if (st != KB_OK) return st;
   if (N == 0) return ok();
   if (!h || !W || !b || !out_token || !out_logit) return fail(KB_ERR_INVALID_ARG, "null input or output pointer");
@@ -455,7 +485,7 @@ int kb_argmax_step(int dtype, int N, int H, int V, const void* h, const void* W,
   return ok();
 }
 
-int kb_beam_finish(int S, int k, int t, int T, int eos, const int32_t* token, const int32_t* parent,
+kb_status kb_beam_finish(int S, int k, int t, int T, int eos, const int32_t* token, const int32_t* parent,
                    const float* score, const int32_t* sent_id, int32_t* beam, const int32_t* prev_keep,
                    int prev_hist_base, int hist_base, int32_t* hist_token, int32_t* hist_parent, int32_t* fin_count,
                    float* fin_score, int32_t* fin_len, int32_t* fin_hist, uint8_t* alive, void* stream) {
@@ -474,7 +504,7 @@ int kb_beam_finish(int S, int k, int t, int T, int eos, const int32_t* token, co
   return ok();
 }
 
-int kb_beam_backtrace(int S0, int k, int T, float alpha, const int32_t* fin_count, const float* fin_score,
+kb_status kb_beam_backtrace(int S0, int k, int T, float alpha, const int32_t* fin_count, const float* fin_score,
                       const int32_t* fin_len, const int32_t* fin_hist, const int32_t* hist_token,
                       const int32_t* hist_parent, int32_t* out_tokens, int32_t* out_len, float* out_score,
                       float* out_norm, void* stream) {
@@ -490,8 +520,36 @@ int kb_beam_backtrace(int S0, int k, int T, float alpha, const int32_t* fin_coun
   return ok();
 }
 
-int kb_compact_batch(int S, int k, const uint8_t* alive, int32_t* keep_idx, int32_t* kept_count,
-                     int32_t* new_sent_offsets, int32_t* kept_sentence, int32_t* new_S, void* stream) {
+size_t kb_compact_workspace_bytes(int M) { return M > 0 ? kb::compact_entries_ws_bytes(M) : 0; }
+
+kb_status kb_compact_batch(int M, const uint8_t* alive_mask, int32_t* keep_idx, int32_t* kept_count,
+                           const int32_t* entry_sentence, int32_t* new_sent_offsets, int32_t* new_S, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  if (M < 0) return fail(KB_ERR_INVALID_ARG, "M = %d < 0", M);
+  if (!kept_count || (M > 0 && (!alive_mask || !keep_idx)))
+    return fail(KB_ERR_INVALID_ARG, "null alive_mask, keep_idx or kept_count");
+  if ((new_sent_offsets || new_S) && !entry_sentence && M > 0)
+    return fail(KB_ERR_INVALID_ARG, "new_sent_offsets and new_S need entry_sentence");
+  const size_t need = kb_compact_workspace_bytes(M);
+  if (need > 0) {
+    if (!workspace) return fail(KB_ERR_WORKSPACE, "workspace is null (%zu bytes needed)", need);
+    if (!aligned(workspace, 4)) return fail(KB_ERR_WORKSPACE, "workspace must be 4-byte aligned");
+    if (workspace_bytes < need) return fail(KB_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, need);
+  }
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  if (entry_sentence && M > 0 && debug_checks()) {
+    kb_status st = debug_verdict(kb::launch_check_sorted(M, entry_sentence, kept_count, hs), kept_count, hs,
+                                 "entry_sentence must be >= 0 and non-decreasing");
+    if (st != KB_OK) return st;
+  }
+  hipError_t e = kb::launch_compact_entries(M, alive_mask, keep_idx, kept_count, entry_sentence, new_sent_offsets,
+                                            new_S, workspace, hs);
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "compaction kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+kb_status kb_compact_beams(int S, int k, const uint8_t* alive, int32_t* keep_idx, int32_t* kept_count,
+                           int32_t* new_sent_offsets, int32_t* kept_sentence, int32_t* new_S, void* stream) {
   if (S < 0) return fail(KB_ERR_INVALID_ARG, "S = %d < 0", S);
   if (k < 1 || k > 1023) return fail(KB_ERR_INVALID_ARG, "k = %d outside [1, 1023]", k);
   if ((long long)S * k > INT_MAX) return fail(KB_ERR_UNSUPPORTED, "S * k too large");
@@ -503,7 +561,7 @@ int kb_compact_batch(int S, int k, const uint8_t* alive, int32_t* keep_idx, int3
   return ok();
 }
 
-int kb_gather_rows(int n_max, const int32_t* n_dev, const int32_t* idx, const void* src, void* dst,
+kb_status kb_gather_rows(int n_max, const int32_t* n_dev, const int32_t* idx, const void* src, void* dst,
                    size_t row_bytes, void* stream) {
   if (n_max < 0) return fail(KB_ERR_INVALID_ARG, "n_max = %d < 0", n_max);
   if (row_bytes == 0 || row_bytes % 4 != 0) return fail(KB_ERR_INVALID_ARG, "row_bytes must be a positive multiple of 4");
@@ -517,10 +575,10 @@ int kb_gather_rows(int n_max, const int32_t* n_dev, const int32_t* idx, const vo
 }
 
 // ---- vocabulary shards (Algorithm 6 across devices): one GPU's part
-int kb_shard_splits(int dtype, int N, int H, int V_shard, int k, const void* h, const void* W_shard,
+kb_status kb_shard_splits(int dtype, int N, int H, int V_shard, int k, const void* h, const void* W_shard,
                     const float* b_shard, int* splits) {
   if (!splits) return fail(KB_ERR_INVALID_ARG, "splits is null");
-  int st = validate_step(dtype, N, H, V_shard, k, N > 0 ? 1 : 0);
+  kb_status st = validate_step(dtype, N, H, V_shard, k, N > 0 ? 1 : 0);
   if (st != KB_OK) return st;
   if (N == 0) {
     *splits = 0;
@@ -536,10 +594,10 @@ size_t kb_shard_workspace_bytes(int dtype, int N, int H, int V_shard, int k) {
   return workspace_bytes(dtype, N, H, V_shard, k);
 }
 
-int kb_shard_partials(int dtype, int N, int H, int V_shard, int word_base, int k, const void* h,
+kb_status kb_shard_partials(int dtype, int N, int H, int V_shard, int word_base, int k, const void* h,
                       const void* W_shard, const float* b_shard, float* stats, int32_t* lists, void* workspace,
                       size_t workspace_bytes, void* stream) {
-  int st = validate_step(dtype, N, H, V_shard, k, N > 0 ? 1 : 0);
+  kb_status st = validate_step(dtype, N, H, V_shard, k, N > 0 ? 1 : 0);
   if (st != KB_OK) return st;
   if (N == 0) return ok();
   if (!h || !W_shard || !b_shard || !stats || !lists) return fail(KB_ERR_INVALID_ARG, "null input or output pointer");
@@ -557,7 +615,7 @@ int kb_shard_partials(int dtype, int N, int H, int V_shard, int word_base, int k
   return ok();
 }
 
-int kb_merge_partials(int N, int V, int k, int S, int P, const float* stats, const int32_t* lists,
+kb_status kb_merge_partials(int N, int V, int k, int S, int P, const float* stats, const int32_t* lists,
                       const float* prev_score, const int32_t* sent_offsets, int32_t* out_token, int32_t* out_parent,
                       float* out_score, float* out_row_lse, void* stream) {
   if (N < 0 || S < 0) return fail(KB_ERR_INVALID_ARG, "negative N (%d) or S (%d)", N, S);
@@ -566,11 +624,13 @@ int kb_merge_partials(int N, int V, int k, int S, int P, const float* stats, con
   if (V < 1) return fail(KB_ERR_INVALID_ARG, "V = %d must be >= 1", V);
   if (k < 1 || k > KB_MAX_K || k > V) return fail(KB_ERR_INVALID_ARG, "k = %d outside [1, min(%d, V = %d)]", k, KB_MAX_K, V);
   if (P < 1 || P > 256) return fail(KB_ERR_UNSUPPORTED, "P = %d splits outside [1, 256]", P);
-  if ((long long)N * k * P > INT_MAX || (long long)N * V > (1LL << 46)) return fail(KB_ERR_UNSUPPORTED, "shape too large");
+  if ((long long)N * k * P > INT_MAX || (long long)N * V > INT_MAX) return fail(KB_ERR_UNSUPPORTED, "shape too large");
   if (N == 0) return ok();
   if (!stats || !lists || !prev_score || !sent_offsets || !out_token || !out_parent || !out_score)
     return fail(KB_ERR_INVALID_ARG, "null input or output pointer");
   if (!aligned(stats, 8) || !aligned(lists, 8)) return fail(KB_ERR_INVALID_ARG, "stats and lists must be 8-byte aligned");
+  kb_status st = debug_offsets(S, N, sent_offsets, out_token, reinterpret_cast<hipStream_t>(stream));
+  if (st != KB_OK) return st;
   kb::K2Args a2{};
   a2.stats = reinterpret_cast<const float2*>(stats);
   a2.lists = reinterpret_cast<const int2*>(lists);
@@ -590,7 +650,7 @@ int kb_merge_partials(int N, int V, int k, int S, int P, const float* stats, con
   return ok();
 }
 
-int kb_standin_alive(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
+kb_status kb_standin_alive(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
                      uint8_t* alive, void* stream) {
   if (S < 0 || k < 1) return fail(KB_ERR_INVALID_ARG, "S = %d, k = %d", S, k);
   if ((long long)S * k > INT_MAX) return fail(KB_ERR_UNSUPPORTED, "S*k does not fit in int32");
@@ -602,7 +662,7 @@ int kb_standin_alive(int S, const int32_t* S_dev, int k, int t, const int32_t* s
   return ok();
 }
 
-int kb_standin_next_h(int n_max, const int32_t* n_dev, int k, int T, int t, const int32_t* keep, const int32_t* sid,
+kb_status kb_standin_next_h(int n_max, const int32_t* n_dev, int k, int T, int t, const int32_t* keep, const int32_t* sid,
                       const void* table, void* out, size_t row_bytes, void* stream) {
   if (n_max < 0 || k < 1 || T < 1 || t < 0 || t >= T)
     return fail(KB_ERR_INVALID_ARG, "n_max = %d, k = %d, T = %d, t = %d", n_max, k, T, t);

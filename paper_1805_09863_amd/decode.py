@@ -112,7 +112,7 @@ def decode_loop(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, lengths
                            out=(tok[:S * k].view(S, k), par[:S * k].view(S, k), sc[:S * k].view(S, k)),
                            ws=ws, stream=stream)
             kbb.standin_alive(sid, lengths, S, k, t, out=alive, S_dev=S_ex, stream=stream)
-            kbb.compact_batch(alive[:S * k], S, k, out=(keep, c[0:1], noff, ksent, c[1:2]), stream=stream)
+            kbb.compact_beams(alive[:S * k], S, k, out=(keep, c[0:1], noff, ksent, c[1:2]), stream=stream)
             with torch.cuda.stream(stream):              # the copy runs on the loop's stream
                 cnt_host[t % 2].copy_(c, non_blocking=True)
             ready[t % 2].record(stream)
@@ -181,7 +181,7 @@ def beam_search(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, k: int,
     at step t, the decoder stand-in.  Every sentence starts from one hypothesis
     (slot 0, score 0) with a beam of k.  Each step: the output layer
     (kb_kbest_step), kb_beam_finish (history, finished store, beam shrink),
-    kb_compact_batch, the gathers of the surviving scores, sentence ids and
+    kb_compact_beams, the gathers of the surviving scores, sentence ids and
     beam sizes, and the stand-in's next states; then one wait for the two
     counts.  A sentence ends when its beam is empty; step T - 1 finishes every
     hypothesis left.  kb_beam_backtrace then picks each sentence's translation
@@ -241,7 +241,7 @@ def beam_search(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, k: int,
                             score=sc[:S * k].view(S, k), alive=alive[:S * k],
                             prev_keep=keep[1 - cur][:N] if t > 0 else None, prev_base=prev_base, base=base,
                             hist_token=hist_tok, hist_parent=hist_par, fin=fin, S=S, N=N))
-        kbb.compact_batch(alive[:S * k], S, k, out=(keep[cur], cnt[0:1], noff, ksent, cnt[1:2]), stream=stream)
+        kbb.compact_beams(alive[:S * k], S, k, out=(keep[cur], cnt[0:1], noff, ksent, cnt[1:2]), stream=stream)
         with torch.cuda.stream(stream):                # the copy runs on the loop's stream
             cnt_host.copy_(cnt, non_blocking=True)
         ready.record(stream)

@@ -53,7 +53,7 @@ def test_standin_argument_checks():
 
 def test_abi_version_and_status_strings():
     L = binding.lib()
-    assert L.kb_abi_version() == 1
+    assert L.kb_abi_version() == 2
     for s in range(5):
         assert L.kb_status_string(s)
     assert L.kb_status_string(99) == b"unknown status"
@@ -103,13 +103,49 @@ def test_empty_batch_is_noop():
     assert L.kb_last_error() == b""
 
 
-def test_compact_validation():
+def test_compact_beams_validation():
     L = binding.lib()
-    assert L.kb_compact_batch(-1, 5, FAKE, FAKE, FAKE, None, None, None, None) == KB_ERR_INVALID_ARG
-    assert L.kb_compact_batch(4, 0, FAKE, FAKE, FAKE, None, None, None, None) == KB_ERR_INVALID_ARG
-    assert L.kb_compact_batch(4, 5, None, FAKE, FAKE, None, None, None, None) == KB_ERR_INVALID_ARG
-    assert L.kb_compact_batch(4, 5, FAKE, FAKE, None, None, None, None, None) == KB_ERR_INVALID_ARG
-    assert L.kb_compact_batch(1 << 30, 8, FAKE, FAKE, FAKE, None, None, None, None) == KB_ERR_UNSUPPORTED
+    assert L.kb_compact_beams(-1, 5, FAKE, FAKE, FAKE, None, None, None, None) == KB_ERR_INVALID_ARG
+    assert L.kb_compact_beams(4, 0, FAKE, FAKE, FAKE, None, None, None, None) == KB_ERR_INVALID_ARG
+    assert L.kb_compact_beams(4, 5, None, FAKE, FAKE, None, None, None, None) == KB_ERR_INVALID_ARG
+    assert L.kb_compact_beams(4, 5, FAKE, FAKE, None, None, None, None, None) == KB_ERR_INVALID_ARG
+    assert L.kb_compact_beams(1 << 30, 8, FAKE, FAKE, FAKE, None, None, None, None) == KB_ERR_UNSUPPORTED
+
+
+def test_compact_batch_validation_and_workspace():
+    L = binding.lib()
+    # one workgroup up to 16,384 entries: no workspace; beyond, two counts per
+    # 4,096 entries and two totals, rounded to 256 bytes
+    assert L.kb_compact_workspace_bytes(0) == 0
+    assert L.kb_compact_workspace_bytes(16384) == 0
+    assert L.kb_compact_workspace_bytes(16385) == 256
+    assert L.kb_compact_workspace_bytes(1 << 24) == ((2 * 4096 + 2) * 4 + 255) // 256 * 256
+    cb = L.kb_compact_batch   # (M, alive, keep, kept, es, new_off, new_S, ws, ws_bytes, stream)
+    assert cb(-1, FAKE, FAKE, FAKE, None, None, None, None, 0, None) == KB_ERR_INVALID_ARG
+    assert cb(10, None, FAKE, FAKE, None, None, None, None, 0, None) == KB_ERR_INVALID_ARG
+    assert cb(10, FAKE, None, FAKE, None, None, None, None, 0, None) == KB_ERR_INVALID_ARG
+    assert cb(10, FAKE, FAKE, None, None, None, None, None, 0, None) == KB_ERR_INVALID_ARG
+    # sentence outputs need the entries' sentence ids
+    assert cb(10, FAKE, FAKE, FAKE, None, FAKE, None, None, 0, None) == KB_ERR_INVALID_ARG
+    assert cb(10, FAKE, FAKE, FAKE, None, None, FAKE, None, 0, None) == KB_ERR_INVALID_ARG
+    # past one workgroup the workspace is required and checked
+    assert cb(20000, FAKE, FAKE, FAKE, None, None, None, None, 0, None) == KB_ERR_WORKSPACE
+    assert cb(20000, FAKE, FAKE, FAKE, None, None, None, FAKE, 16, None) == KB_ERR_WORKSPACE
+    assert cb(20000, FAKE, FAKE, FAKE, None, None, None, ctypes.c_void_p(0x1002), 1 << 20, None) == KB_ERR_WORKSPACE
+    assert L.kb_last_error()
+
+
+def test_size_limits_are_reported_unsupported():
+    L = binding.lib()
+    # a sentence's flat index (row * V + word) must be an int32
+    assert _step(L, dtype=1, N=23861, H=128, V=90000, k=5, S=1) == KB_ERR_UNSUPPORTED
+    assert b"INT_MAX" in L.kb_last_error()
+    assert L.kb_kbest_workspace_bytes(1, 23861, 128, 90000, 5, 1) == 0
+    # h of 4 GiB or more (32-bit byte offsets)
+    assert _step(L, dtype=1, N=1 << 20, H=2048, V=16, k=5, S=1) == KB_ERR_UNSUPPORTED
+    assert _step(L, dtype=0, N=1 << 20, H=1024, V=16, k=5, S=1) == KB_ERR_UNSUPPORTED
+    mp = L.kb_merge_partials
+    assert mp(23861, 90000, 5, 1, 4, *([FAKE] * 7), None, None) == KB_ERR_UNSUPPORTED
 
 
 def test_gather_validation():
@@ -210,4 +246,82 @@ def test_host_tensors_are_refused_not_computed():
     with pytest.raises(TypeError, match="on the GPU"):
         kb.kbest_step(h, W, b, prev, off, 3)
     with pytest.raises(TypeError, match="on the GPU"):
-        kb.compact_batch(torch.ones(10, dtype=torch.uint8), 2, 5)
+        kb.compact_beams(torch.ones(10, dtype=torch.uint8), 2, 5)
+    with pytest.raises(TypeError, match="on the GPU"):
+        kb.compact_batch(torch.ones(10, dtype=torch.uint8))
+
+
+class _FakeLib:
+    """Stands in for libkbest: every entry point succeeds without touching memory."""
+
+    def __getattr__(self, name):
+        if name.endswith("_workspace_bytes"):
+            return lambda *a: 4096
+        if name == "kb_shard_splits":
+            def splits(*a):
+                a[-1]._obj.value = 2
+                return 0
+            return splits
+        if name == "kb_last_error":
+            return lambda: b""
+        return lambda *a: 0
+
+
+def _fake_stream():
+    class S:
+        cuda_stream = 0
+    return S()
+
+
+def test_every_pointer_the_binding_passes_was_checked(monkeypatch):
+    # each tensor whose address reaches the library has been through the
+    # binding's check (device, layout, type and size) first: output tensors,
+    # workspaces and optional arrays included, not only the inputs
+    import torch
+    checked, passed = set(), []
+    monkeypatch.setattr(binding, "_lib", _FakeLib())
+    monkeypatch.setattr(binding, "_need", lambda t, *a, **k: checked.add(id(t)))
+    real_ptr = binding._ptr
+
+    def ptr(t):
+        if t is not None:
+            passed.append(t)
+        return real_ptr(t)
+    monkeypatch.setattr(binding, "_ptr", ptr)
+    st = _fake_stream()
+    f32, i32, u8, bf = torch.float32, torch.int32, torch.uint8, torch.bfloat16
+    z = lambda *shape, d=f32: torch.zeros(shape, dtype=d)     # noqa: E731
+    N, H, V, k, S = 6, 16, 40, 3, 2
+    h, W, b, prev, off = z(N, H, d=bf), z(H, V, d=bf), z(V), z(N), torch.tensor([0, 3, 6], dtype=i32)
+    out3 = (z(S, k, d=i32), z(S, k, d=i32), z(S, k))
+    binding.kbest_step(h, W, b, prev, off, k, out=out3, ws=z(4096, d=u8), row_lse=z(N), stream=st)
+    binding.argmax_step(h, W, b, out=(z(N, d=i32), z(N)), ws=z(4096, d=u8), stream=st)
+    binding.kbest_step_unfused(h, W, b, prev, off, k, out=out3, ws=z(4096, d=u8), row_lse=z(N), stream=st)
+    binding.compact_batch(z(10, d=u8), torch.arange(10, dtype=i32) // 3,
+                          out=(z(10, d=i32), z(1, d=i32), z(11, d=i32), z(1, d=i32)), ws=z(4096, d=u8), stream=st)
+    binding.compact_beams(z(S * k, d=u8), S, k, out=(z(S * k, d=i32), z(1, d=i32), z(S + 1, d=i32), z(S, d=i32),
+                                                    z(1, d=i32)), stream=st)
+    binding.gather_rows(z(10, 4), torch.arange(5, dtype=i32), n_dev=z(1, d=i32), out=z(5, 4), stream=st)
+    stats, lists = z(2 * N * 2), z(2 * N * k * 2, d=i32)
+    binding.shard_partials(h, W, b, k, 0, stats, lists, ws=z(4096, d=u8), stream=st)
+    binding.merge_partials(stats, lists, 2, V, k, prev, off, out=out3, row_lse=z(N), stream=st)
+    binding.standin_alive(z(S, d=i32), z(4, d=i32), S, k, 0, out=z(S * k, d=u8), S_dev=z(1, d=i32), stream=st)
+    binding.standin_next_h(z(40, H, d=bf), z(S * k, d=i32), z(S, d=i32), k, 4, 1, S * k, n_dev=z(1, d=i32),
+                           out=z(S * k, H, d=bf), stream=st)
+    fin = (z(4, d=i32), z(4 * k), z(4 * k, d=i32), z(4 * k, d=i32))
+    binding.beam_finish(S, k, 0, 4, 1, out3[0], out3[1], out3[2], z(S, d=i32), z(S, d=i32), z(S, d=i32), 0, 0,
+                        z(4 * S * k, d=i32), z(4 * S * k, d=i32), fin, z(S * k, d=u8), stream=st)
+    binding.beam_backtrace(4, k, 4, 1.0, fin, z(4 * S * k, d=i32), z(4 * S * k, d=i32),
+                           out=(z(4, 4, d=i32), z(4, d=i32), z(4), z(4)), stream=st)
+    unchecked = [tuple(t.shape) for t in passed if id(t) not in checked]
+    assert passed and not unchecked, f"pointers passed without a check: {unchecked}"
+
+
+def test_output_and_workspace_checks_raise():
+    import torch
+    # the checks themselves: host tensors, short outputs, small workspaces
+    with pytest.raises(TypeError, match="on the GPU"):
+        binding._need_outs((torch.zeros(4, dtype=torch.int32),), ("token",), (torch.int32,), 4)
+    with pytest.raises(TypeError, match="on the GPU"):
+        binding._need_ws(torch.zeros(64, dtype=torch.uint8), 16)
+

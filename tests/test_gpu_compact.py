@@ -48,7 +48,7 @@ def test_compact_bit_exact(kb, pattern, S, k):
     g = np.random.default_rng(S * 31 + k)
     a = _mask(pattern, S, k, g)
     say(f"compact S={S} k={k} {pattern}")
-    keep, kept, noff, ksent, nS = kb.compact_batch(torch.from_numpy(a).cuda(), S, k)
+    keep, kept, noff, ksent, nS = kb.compact_beams(torch.from_numpy(a).cuda(), S, k)
     torch.cuda.synchronize()
     ref = ko.compact(a != 0, S, k)
     n = int(kept.item())
@@ -68,7 +68,7 @@ def test_compact_empty_batch(kb):
     noff = torch.full((1,), -7, dtype=torch.int32, device="cuda")
     ksent = torch.full((1,), -7, dtype=torch.int32, device="cuda")
     nS = torch.full((1,), -7, dtype=torch.int32, device="cuda")
-    kb.compact_batch(torch.zeros(0, dtype=torch.uint8, device="cuda"), 0, 5, out=(keep, kept, noff, ksent, nS))
+    kb.compact_beams(torch.zeros(0, dtype=torch.uint8, device="cuda"), 0, 5, out=(keep, kept, noff, ksent, nS))
     torch.cuda.synchronize()
     assert kept.item() == 0 and nS.item() == 0 and noff.item() == 0 and keep.item() == -7
 
@@ -107,3 +107,115 @@ def test_standin_alive_device_count(kb, S_live):
     torch.cuda.synchronize()
     want = np.repeat((np.arange(S) < live) & (t < lengths[sid] - 1), k).astype(np.uint8)
     assert np.array_equal(alive.cpu().numpy(), want)
+
+
+# ---------------------------------------------------------------- the M-entry form (kb_compact_batch)
+def _entries(M, g, max_sent=6):
+    sizes = []
+    while sum(sizes) < M:
+        sizes.append(int(g.integers(0, max_sent + 1)))        # empty sentences included
+    es = np.repeat(np.arange(len(sizes)), sizes)[:M]
+    return (es + 3).astype(np.int32)                          # ids need not start at 0
+
+
+@pytest.mark.parametrize("M", [0, 1, 7, 4096, 4097, 16384, 16385, 100_003, 1_000_000])
+@pytest.mark.parametrize("pattern", ["random", "none", "all", "sparse"])
+def test_compact_batch_entries_bit_exact(kb, M, pattern):
+    # one workgroup up to 16,384 entries, the three-kernel form past that
+    # (ragged last workgroup, several workgroups in the count scan)
+    g = np.random.default_rng(M + len(pattern))
+    a = {"random": g.random(M) < 0.5, "none": np.zeros(M, bool), "all": np.ones(M, bool),
+         "sparse": g.random(M) < 0.002}[pattern].astype(np.uint8) * np.uint8(g.integers(1, 200))
+    es = _entries(M, g)
+    say(f"compact_batch M={M} {pattern}: {int((a != 0).sum())} alive")
+    alive = torch.from_numpy(a).cuda()
+    es_d = torch.from_numpy(es).cuda()
+    keep = torch.full((max(M, 1),), -5, dtype=torch.int32, device="cuda")
+    kept = torch.full((1,), -5, dtype=torch.int32, device="cuda")
+    noff = torch.full((M + 1,), -5, dtype=torch.int32, device="cuda")
+    nS = torch.full((1,), -5, dtype=torch.int32, device="cuda")
+    kb.compact_batch(alive, es_d, out=(keep, kept, noff, nS))
+    torch.cuda.synchronize()
+    ref = ko.compact_entries(a, es)
+    n, ns = int(kept.item()), int(nS.item())
+    assert n == ref.kept_count and ns == ref.new_S
+    assert np.array_equal(keep.cpu().numpy()[:n], ref.keep_idx)
+    assert np.array_equal(noff.cpu().numpy()[:ns + 1], ref.new_offsets)
+    assert (noff.cpu().numpy()[ns + 1:] == -5).all()          # nothing written past new_S
+    # without sentence ids: the kept list only
+    keep2, kept2, noff2, nS2 = kb.compact_batch(alive)
+    torch.cuda.synchronize()
+    assert noff2 is None and nS2 is None
+    assert int(kept2.item()) == n and np.array_equal(keep2.cpu().numpy()[:n], ref.keep_idx)
+
+
+def test_compact_batch_matches_beam_form(kb):
+    # an S x k batch with entry_sentence = i // k gives the S x k form's results
+    g = np.random.default_rng(12)
+    S, k = 900, 5
+    a = (g.random(S * k) < 0.4).astype(np.uint8)
+    alive = torch.from_numpy(a).cuda()
+    es = torch.arange(S * k, dtype=torch.int32, device="cuda") // k
+    keep, kept, noff, nS = kb.compact_batch(alive, es)
+    keep_b, kept_b, noff_b, ksent_b, nS_b = kb.compact_beams(alive, S, k)
+    torch.cuda.synchronize()
+    n, ns = int(kept.item()), int(nS.item())
+    assert n == int(kept_b.item()) and ns == int(nS_b.item())
+    assert torch.equal(keep[:n], keep_b[:n]) and torch.equal(noff[:ns + 1], noff_b[:ns + 1])
+
+
+# ---------------------------------------------------------------- KB_DEBUG validation
+def _small_step_inputs(S=4, beam=3, V=900, H=64):
+    from synth import workloads as wl
+    from tests.gpu_util import to_dev
+    inp = wl.make_step(H=H, V=V, k=4, S=S, beam=beam, dtype="f32", seed=3, name="dbg")
+    return inp, to_dev(inp)
+
+
+@pytest.mark.parametrize("bad", ["first", "decreasing", "past_N"])
+def test_debug_rejects_bad_sentence_offsets(kb, monkeypatch, bad):
+    inp, (h, W, b, prev, off) = _small_step_inputs()
+    o = inp.off.copy()
+    if bad == "first":
+        o[0] = 1
+    elif bad == "decreasing":
+        o[2], o[3] = o[3], o[2]
+    else:
+        o[-1] = inp.N + 1
+    off_bad = torch.from_numpy(o).cuda()
+    tok = torch.full((inp.S, inp.k), 123, dtype=torch.int32, device="cuda")
+    par = torch.full((inp.S, inp.k), 123, dtype=torch.int32, device="cuda")
+    sc = torch.full((inp.S, inp.k), 1.5, dtype=torch.float32, device="cuda")
+    monkeypatch.setenv("KB_DEBUG", "1")
+    with pytest.raises(kb.KBestError) as e:
+        kb.kbest_step(h, W, b, prev, off_bad, inp.k, out=(tok, par, sc))
+    assert e.value.status == 1 and "KB_DEBUG" in str(e.value)
+    torch.cuda.synchronize()
+    # nothing but the verdict word was written: no merge ran
+    assert (par == 123).all() and (sc == 1.5).all() and (tok.view(-1)[1:] == 123).all()
+    # the same offsets through the vocabulary-shard merge
+    stats = torch.zeros((1, inp.N, 2), dtype=torch.float32, device="cuda")
+    lists = torch.zeros((1, inp.N, inp.k, 2), dtype=torch.int32, device="cuda")
+    with pytest.raises(kb.KBestError) as e:
+        kb.merge_partials(stats, lists, 1, inp.V, inp.k, prev, off_bad)
+    assert e.value.status == 1
+    # valid offsets pass under KB_DEBUG and give the usual result
+    t1, p1, s1 = kb.kbest_step(h, W, b, prev, off, inp.k)
+    monkeypatch.delenv("KB_DEBUG")
+    t0, p0, s0 = kb.kbest_step(h, W, b, prev, off, inp.k)
+    torch.cuda.synchronize()
+    assert torch.equal(t0, t1) and torch.equal(p0, p1) and torch.equal(s0, s1)
+
+
+def test_debug_rejects_unsorted_entry_sentences(kb, monkeypatch):
+    alive = torch.ones(10, dtype=torch.uint8, device="cuda")
+    es = torch.tensor([0, 0, 1, 1, 2, 1, 3, 3, 4, 4], dtype=torch.int32, device="cuda")
+    monkeypatch.setenv("KB_DEBUG", "1")
+    with pytest.raises(kb.KBestError) as e:
+        kb.compact_batch(alive, es)
+    assert e.value.status == 1
+    with pytest.raises(kb.KBestError):
+        kb.compact_batch(alive, torch.full((10,), -1, dtype=torch.int32, device="cuda"))
+    keep, kept, noff, nS = kb.compact_batch(alive, torch.sort(es).values.contiguous())
+    torch.cuda.synchronize()
+    assert int(kept.item()) == 10 and int(nS.item()) == 5

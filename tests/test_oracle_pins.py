@@ -415,3 +415,40 @@ def test_exhaustive_compaction_small():
             keep, off, ks = _compact_loop(list(bits), S, k)
             assert res.keep_idx.tolist() == keep and res.new_offsets.tolist() == off
             assert res.kept_sentence.tolist() == ks
+
+
+def _compact_entries_loop(alive, es):
+    # the batch walked entry by entry: a sentence opens when its first
+    # surviving entry is met
+    keep, off, ks = [], [], []
+    for i, a in enumerate(alive):
+        if a:
+            if not ks or ks[-1] != es[i]:
+                ks.append(es[i])
+                off.append(len(keep))
+            keep.append(i)
+    off.append(len(keep))
+    return keep, off, ks
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_compact_entries_matches_loop(seed):
+    g = np.random.default_rng(300 + seed)
+    sizes = g.integers(0, 7, g.integers(1, 40))          # empty sentences included
+    es = np.repeat(np.arange(sizes.size), sizes)
+    a = (g.random(es.size) < [0.0, 0.3, 0.5, 0.9, 1.0, 0.5][seed]).astype(np.uint8)
+    res = ko.compact_entries(a, es)
+    keep, off, ks = _compact_entries_loop(a.tolist(), es.tolist())
+    assert res.keep_idx.tolist() == keep and res.kept_count == len(keep)
+    assert res.new_offsets.tolist() == off and res.kept_sentence.tolist() == ks and res.new_S == len(ks)
+    bare = ko.compact_entries(a)
+    assert bare.keep_idx.tolist() == keep and bare.kept_count == len(keep)
+
+
+def test_compact_entries_exhaustive_small():
+    for es in ([0, 0, 1], [0, 1, 1, 3], [2, 2, 2], [0, 1, 2, 3]):
+        for bits in itertools.product([0, 1], repeat=len(es)):
+            res = ko.compact_entries(np.array(bits, np.uint8), np.array(es))
+            keep, off, ks = _compact_entries_loop(list(bits), es)
+            assert res.keep_idx.tolist() == keep and res.new_offsets.tolist() == off
+            assert res.kept_sentence.tolist() == ks
