@@ -460,15 +460,15 @@ def beam_finish(S: int, k: int, t: int, T: int, eos: int, token, parent, score, 
     (count, score, len, hist), shrink the beams and fill ``alive`` (include/kbest.h)."""
     fc, fs, fl, fh = fin
     n = S * k
-    for t, nm, d, m in ((token, "token", torch.int32, n), (parent, "parent", torch.int32, n),
+    for x, nm, d, m in ((token, "token", torch.int32, n), (parent, "parent", torch.int32, n),
                         (score, "score", torch.float32, n), (sent_id, "sent_id", torch.int32, S),
                         (beam, "beam", torch.int32, S), (hist_token, "hist_token", torch.int32, hist_base + n),
                         (hist_parent, "hist_parent", torch.int32, hist_base + n),
                         (fc, "fin_count", torch.int32, S), (alive, "alive", torch.uint8, n)):
-        _need(t, nm, dtype=d, numel=m)
+        _need(x, nm, dtype=d, numel=m)
     S0 = fc.numel()             # the finished store holds k slots per original sentence
-    for t, nm, d in ((fs, "fin_score", torch.float32), (fl, "fin_len", torch.int32), (fh, "fin_hist", torch.int32)):
-        _need(t, nm, dtype=d, numel=S0 * k)
+    for x, nm, d in ((fs, "fin_score", torch.float32), (fl, "fin_len", torch.int32), (fh, "fin_hist", torch.int32)):
+        _need(x, nm, dtype=d, numel=S0 * k)
     if prev_keep is not None:
         _need(prev_keep, "prev_keep", dtype=torch.int32, numel=S)
     _check(lib().kb_beam_finish(S, k, t, T, eos, _ptr(token), _ptr(parent), _ptr(score), _ptr(sent_id), _ptr(beam),
@@ -485,9 +485,9 @@ def beam_backtrace(S0: int, k: int, T: int, alpha: float, fin: tuple, hist_token
     if out is None:
         out = (torch.empty((S0, T), dtype=torch.int32, device=dev), torch.empty(S0, dtype=torch.int32, device=dev),
                torch.empty(S0, dtype=torch.float32, device=dev), torch.empty(S0, dtype=torch.float32, device=dev))
-    for t, nm_, d in ((fc, "fin_count", torch.int32), (fs, "fin_score", torch.float32),
+    for x, nm_, d in ((fc, "fin_count", torch.int32), (fs, "fin_score", torch.float32),
                       (fl, "fin_len", torch.int32), (fh, "fin_hist", torch.int32)):
-        _need(t, nm_, dtype=d, numel=S0 * (1 if nm_ == "fin_count" else k))
+        _need(x, nm_, dtype=d, numel=S0 * (1 if nm_ == "fin_count" else k))
     _need(hist_token, "hist_token", dtype=torch.int32)
     _need(hist_parent, "hist_parent", dtype=torch.int32)
     _need_outs(out[:1], ("tokens",), (torch.int32,), S0 * T)

@@ -252,19 +252,31 @@ def test_host_tensors_are_refused_not_computed():
 
 
 class _FakeLib:
-    """Stands in for libkbest: every entry point succeeds without touching memory."""
+    """Stands in for libkbest: every entry point succeeds without touching memory,
+    after checking the arguments against the declared signature (count, and
+    that each integer, size, float and pointer slot gets a value of that kind)."""
 
     def __getattr__(self, name):
-        if name.endswith("_workspace_bytes"):
-            return lambda *a: 4096
-        if name == "kb_shard_splits":
-            def splits(*a):
+        res, argtypes = binding.SIGNATURES[name]
+
+        def call(*a):
+            assert len(a) == len(argtypes), f"{name}: {len(a)} arguments, {len(argtypes)} declared"
+            for i, (v, t) in enumerate(zip(a, argtypes)):
+                if t in (ctypes.c_int, ctypes.c_size_t):
+                    assert isinstance(v, int) and not isinstance(v, bool), f"{name} argument {i}: {v!r}"
+                elif t is ctypes.c_float:
+                    assert isinstance(v, (int, float)), f"{name} argument {i}: {v!r}"
+                else:
+                    assert v is None or isinstance(v, (ctypes.c_void_p, int)) or hasattr(v, "_obj"), \
+                        f"{name} argument {i}: {v!r}"
+            if name.endswith("_workspace_bytes"):
+                return 4096
+            if name == "kb_shard_splits":
                 a[-1]._obj.value = 2
-                return 0
-            return splits
-        if name == "kb_last_error":
-            return lambda: b""
-        return lambda *a: 0
+            if name == "kb_last_error":
+                return b""
+            return 0
+        return call
 
 
 def _fake_stream():
