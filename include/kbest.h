@@ -153,6 +153,30 @@ kb_status kb_kbest_step_events(int dtype, int N, int H, int V, int k, int S,
                          void* proj_begin_event, void* proj_end_event);
 
 /*
+ * kb_kbest_step_noalloc -- kb_kbest_step for callers that cannot allocate
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): no workspace argument.  The projection's partials and shared
+ * row thresholds go to a fixed array of kb_kbest_step_scratch_max() bytes
+ * (16 MiB) in the library's device memory, one per GPU, held from the
+ * library's load on that GPU until the process ends.  The call allocates and
+ * frees nothing; its first call on a device looks up that device's array.
+ *   Arguments, results and errors as kb_kbest_step.  A shape whose
+ *   kb_kbest_workspace_bytes exceeds the array returns KB_ERR_UNSUPPORTED
+ *   (the V = 90,000, N = 3,072, k = 12 step needs 6.9 MB; N = 4,096 with
+ *   k = 16 needs 9.2 MB).
+ * Every call on a GPU shares that GPU's array and leaves its contents behind
+ * (the thresholds are cleared by a kernel at the start of each call): calls
+ * that overlap on one GPU, on different streams or host threads, race and
+ * give undefined results.  Calls on one stream are ordered and safe.
+ */
+size_t kb_kbest_step_scratch_max(void);
+kb_status kb_kbest_step_noalloc(int dtype, int N, int H, int V, int k, int S,
+                                const void* h, const void* W, const float* b,
+                                const float* prev_score, const int32_t* sent_offsets,
+                                int32_t* out_token, int32_t* out_parent, float* out_score,
+                                float* out_row_lse, void* stream);
+
+/*
  * kb_argmax_step -- greedy decoding (beam 1): the best word of every row,
  * without any softmax (Algorithm 5: argmax of p = W h + b; Algorithm 6: the
  * vocabulary is sharded, each shard's (max, best) found in parallel, then

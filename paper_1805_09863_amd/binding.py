@@ -34,6 +34,8 @@ SIGNATURES = {
     "kb_kbest_step": (_I, [_I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "kb_kbest_step_events": (_I, [_I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P,
                                   _P, _P]),
+    "kb_kbest_step_scratch_max": (_SZ, []),
+    "kb_kbest_step_noalloc": (_I, [_I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "kb_argmax_workspace_bytes": (_SZ, [_I, _I, _I, _I]),
     "kb_argmax_step": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "kb_unfused_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I, _I]),
@@ -189,6 +191,35 @@ def kbest_step(h: torch.Tensor, W: torch.Tensor, b: torch.Tensor, prev_score: to
         _check(L.kb_kbest_step(*args))
     else:
         _check(L.kb_kbest_step_events(*args, ctypes.c_void_p(events[0]), ctypes.c_void_p(events[1])))
+    return tok, par, sc
+
+
+def kbest_step_noalloc(h: torch.Tensor, W: torch.Tensor, b: torch.Tensor, prev_score: torch.Tensor,
+                       sent_offsets: torch.Tensor, k: int, *, out: tuple, S: Optional[int] = None,
+                       row_lse: Optional[torch.Tensor] = None, stream=None):
+    """kbest_step without a workspace (include/kbest.h, kb_kbest_step_noalloc): the
+    library's fixed per-device scratch array takes the partials, so nothing is
+    allocated, here or in the library; ``out`` = (token, parent, score) must be given."""
+    _need(h, "h", dim=2)
+    _need(W, "W", dtype=h.dtype, dim=2)
+    _need(b, "b", dtype=torch.float32, dim=1)
+    _need(prev_score, "prev_score", dtype=torch.float32, dim=1)
+    _need(sent_offsets, "sent_offsets", dtype=torch.int32, dim=1)
+    dt = _dtype_code(h)
+    N, H = h.shape
+    H2, V = W.shape
+    if H2 != H or b.shape[0] != V or prev_score.shape[0] != N:
+        raise ValueError("shape mismatch among h, W, b, prev_score")
+    S = sent_offsets.shape[0] - 1 if S is None else S
+    if sent_offsets.shape[0] != S + 1:
+        raise ValueError("sent_offsets must have S+1 entries")
+    _need_outs(out, ("token", "parent", "score"), (torch.int32, torch.int32, torch.float32), S * k)
+    if row_lse is not None:
+        _need(row_lse, "row_lse", dtype=torch.float32, numel=N)
+    tok, par, sc = out
+    _check(lib().kb_kbest_step_noalloc(dt, N, H, V, k, S, _ptr(h), _ptr(W), _ptr(b), _ptr(prev_score),
+                                       _ptr(sent_offsets), _ptr(tok), _ptr(par), _ptr(sc), _ptr(row_lse),
+                                       _stream(stream)))
     return tok, par, sc
 
 

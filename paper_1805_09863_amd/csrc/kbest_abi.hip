@@ -5,6 +5,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 
 #include "kbest.h"
@@ -385,6 +386,59 @@ kb_status kb_kbest_step_events(int dtype, int N, int H, int V, int k, int S, con
   return kbest_step_impl(dtype, N, H, V, k, S, h, W, b, prev_score, sent_offsets, out_token, out_parent,
                          out_score, out_row_lse, workspace, workspace_bytes, stream, proj_begin_event,
                          proj_end_event);
+}
+
+// ---- the step without a caller workspace: the projection's partials and
+// shared thresholds go to a fixed device array of this library instead
+}  // extern "C"
+
+namespace {
+constexpr size_t kScratchBytes = (size_t)16 << 20;
+constexpr int kMaxDevices = 64;
+// One copy per device, held from module load until the process ends.
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+// Device address of `scratch` on the current device, looked up once per
+// device (the array's name is a host-side stand-in, not a device address).
+kb_status scratch_ptr(void** out) {
+  static std::mutex mu;
+  static void* ptrs[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(KB_ERR_UNSUPPORTED, "device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(mu);
+  if (ptrs[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return fail(KB_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    ptrs[dev] = p;
+  }
+  *out = ptrs[dev];
+  return KB_OK;
+}
+}  // namespace
+
+extern "C" {
+
+size_t kb_kbest_step_scratch_max(void) { return kScratchBytes; }
+
+kb_status kb_kbest_step_noalloc(int dtype, int N, int H, int V, int k, int S, const void* h, const void* W,
+                                const float* b, const float* prev_score, const int32_t* sent_offsets,
+                                int32_t* out_token, int32_t* out_parent, float* out_score, float* out_row_lse,
+                                void* stream) {
+  kb_status st = validate_step(dtype, N, H, V, k, S);
+  if (st != KB_OK) return st;
+  if (N == 0) return ok();
+  const size_t need = workspace_bytes(dtype, N, H, V, k);
+  if (need > kScratchBytes)
+    return fail(KB_ERR_UNSUPPORTED, "this shape needs %zu bytes of scratch; the fixed array holds %zu", need,
+                kScratchBytes);
+  void* ws = nullptr;
+  if ((st = scratch_ptr(&ws)) != KB_OK) return st;
+  return kbest_step_impl(dtype, N, H, V, k, S, h, W, b, prev_score, sent_offsets, out_token, out_parent, out_score,
+                         out_row_lse, ws, kScratchBytes, stream, nullptr, nullptr);
 }
 
 
