@@ -111,10 +111,10 @@ def test_standin_alive_device_count(kb, S_live):
 
 # ---------------------------------------------------------------- the M-entry form (kb_compact_batch)
 def _entries(M, g, max_sent=6):
-    sizes = []
-    while sum(sizes) < M:
-        sizes.append(int(g.integers(0, max_sent + 1)))        # empty sentences included
-    es = np.repeat(np.arange(len(sizes)), sizes)[:M]
+    sizes = g.integers(0, max_sent + 1, M + 1)                # empty sentences included
+    es = np.repeat(np.arange(sizes.size), sizes)[:M]          # sum(sizes) >= M unless all draws are 0
+    if es.size < M:
+        es = np.concatenate([es, np.full(M - es.size, sizes.size)])
     return (es + 3).astype(np.int32)                          # ids need not start at 0
 
 
