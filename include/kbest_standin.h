@@ -6,8 +6,8 @@
  * that measures mini-batching (Section 2.1, Algorithm 2 against the constant
  * batch of Algorithm 1) replaces it by a seeded table of states and a drawn
  * length per sentence, at which all of the sentence's continuations end.
- * These two calls keep that bookkeeping on the device, so a loop step needs
- * no host work beyond reading two counts.  Conventions (caller-owned device
+ * These calls keep that bookkeeping on the device, so a loop step needs no
+ * host work beyond reading two counts.  Conventions (caller-owned device
  * buffers, stream ordering, kb_status returns, kb_last_error) are those of
  * kbest.h; the functions live in the same library.
  */
@@ -37,6 +37,36 @@ extern "C" {
  */
 kb_status kb_standin_alive(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
                      uint8_t* alive, void* stream);
+
+/*
+ * kb_standin_step -- the bookkeeping of one loop step after the output layer,
+ * in one launch: the mask of kb_standin_alive, the compaction of
+ * kb_compact_beams over it (the same scan: Section 2.1, Algorithm 2's removal
+ * of finished hypotheses, stable), and the gathers that carry the surviving
+ * entries' scores and the surviving sentences' original ids to the next step.
+ *   S, S_dev, k, t, sid, lengths   as kb_standin_alive (sid is read only for
+ *              sentences below min(S, *S_dev)).
+ *   score      S*k float32, the step's scores (kb_kbest_step's out_score).
+ *   keep_idx   S*k int32 out: the surviving entries in order (first counts[0]).
+ *   counts     2 int32 out: [0] surviving entries, [1] surviving sentences.
+ *   new_sent_offsets  S+1 int32 out: the next batch's offsets; entries past
+ *              counts[1] repeat counts[0] (empty sentences), as kb_compact_beams.
+ *   prev_next  S*k float32 out: prev_next[i] = score[keep_idx[i]], i < counts[0].
+ *   sid_next   S int32 out: the original id of surviving sentence j, j < counts[1].
+ *   alive      NULL or S*k uint8 out: the mask itself.
+ *   counts_host  NULL or 2 int32 of pinned host memory (allocated pinned, so
+ *              the device can write it): the counts again, for a host that
+ *              reads them once the step's work has completed (an event on
+ *              `stream`), without a separate copy.
+ * Buffers are distinct, caller-owned device memory (counts_host aside).  S == 0 writes counts = 0
+ * and new_sent_offsets[0] = 0.  1 <= k < 1024; S*k fits in int32.  One
+ * workgroup does it all (the batches of a decode loop are a few thousand
+ * entries).  KB_ERR_INVALID_ARG for null required pointers or bad sizes.
+ */
+kb_status kb_standin_step(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
+                          const float* score, int32_t* keep_idx, int32_t* counts, int32_t* new_sent_offsets,
+                          float* prev_next, int32_t* sid_next, uint8_t* alive, int32_t* counts_host,
+                          void* stream);
 
 /*
  * kb_standin_next_h -- the states of step t for the entries kept by

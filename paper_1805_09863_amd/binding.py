@@ -54,6 +54,7 @@ SIGNATURES = {
     # decoder stand-in of the synthetic decode loop (include/kbest_standin.h)
     "kb_standin_alive": (_I, [_I, _P, _I, _I, _P, _P, _P, _P]),
     "kb_standin_next_h": (_I, [_I, _P, _I, _I, _I, _P, _P, _P, _P, _SZ, _P]),
+    "kb_standin_step": (_I, [_I, _P, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
 }
 
 
@@ -85,6 +86,11 @@ def _check(status: int):
 
 
 def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _ptr_host(t: Optional[torch.Tensor]):
+    """Address of a pinned host tensor (checked by the caller) that kernels write."""
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
@@ -465,6 +471,39 @@ def standin_alive(sid: torch.Tensor, lengths: torch.Tensor, S: int, k: int, t: i
     if S_dev is not None:
         _need(S_dev, "S_dev", dtype=torch.int32, numel=1)
     _check(lib().kb_standin_alive(S, _ptr(S_dev), k, t, _ptr(sid), _ptr(lengths), _ptr(out), _stream(stream)))
+    return out
+
+
+def standin_step(sid: torch.Tensor, lengths: torch.Tensor, score: torch.Tensor, S: int, k: int, t: int, *,
+                 out: tuple, S_dev: Optional[torch.Tensor] = None, alive: Optional[torch.Tensor] = None,
+                 counts_host: Optional[torch.Tensor] = None, stream=None):
+    """The loop step's bookkeeping in one launch (include/kbest_standin.h): the
+    EOS mask, its compaction and the gathers of the surviving scores and sentence
+    ids.  ``out`` = (keep_idx[S*k], counts[2], new_sent_offsets[S+1],
+    prev_next[S*k] float32, sid_next[S]); returns it.  ``counts_host``, a pinned
+    int32 host tensor of 2, receives the counts too (readable once the step's
+    work has completed)."""
+    keep, counts, noff, prev_next, sid_next = out
+    _need(sid, "sid", dtype=torch.int32, numel=S)
+    _need(lengths, "lengths", dtype=torch.int32)
+    _need(score, "score", dtype=torch.float32, numel=S * k)
+    _need(keep, "keep_idx", dtype=torch.int32, numel=S * k)
+    _need(counts, "counts", dtype=torch.int32, numel=2)
+    _need(noff, "new_sent_offsets", dtype=torch.int32, numel=S + 1)
+    _need(prev_next, "prev_next", dtype=torch.float32, numel=S * k)
+    _need(sid_next, "sid_next", dtype=torch.int32, numel=S)
+    if S_dev is not None:
+        _need(S_dev, "S_dev", dtype=torch.int32, numel=1)
+    if alive is not None:
+        _need(alive, "alive", dtype=torch.uint8, numel=S * k)
+    if counts_host is not None:
+        if not isinstance(counts_host, torch.Tensor) or counts_host.is_cuda or not counts_host.is_pinned():
+            raise TypeError("counts_host must be a pinned host tensor")
+        if counts_host.dtype != torch.int32 or counts_host.numel() < 2 or not counts_host.is_contiguous():
+            raise ValueError("counts_host must be 2 contiguous int32")
+    _check(lib().kb_standin_step(S, _ptr(S_dev), k, t, _ptr(sid), _ptr(lengths), _ptr(score), _ptr(keep),
+                                 _ptr(counts), _ptr(noff), _ptr(prev_next), _ptr(sid_next), _ptr(alive),
+                                 _ptr_host(counts_host), _stream(stream)))
     return out
 
 

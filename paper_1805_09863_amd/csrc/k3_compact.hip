@@ -6,36 +6,9 @@
 // and each survivor writes its index at its rank.  A second pass does the same
 // over sentences with a packed (surviving sentence, surviving entries) count
 // to build the new offsets.  Integer work only: results are exact.
-#include "kb_launch.hpp"
+#include "k3_scan.hpp"
 
 namespace kb {
-
-constexpr int K3_T = 1024;
-constexpr int K3_W = K3_T / 64;
-constexpr int K3_ITEMS = 4;
-
-// Exclusive scan of v over the workgroup; returns the total in *total.
-__device__ __forceinline__ int block_excl_scan(int v, int* wsum, int* total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int x = v;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const int y = __shfl_up(x, d, 64);
-    if (lane >= d) x += y;
-  }
-  __syncthreads();  // wsum is reused between calls
-  if (lane == 63) wsum[wave] = x;
-  __syncthreads();
-  int before = 0, all = 0;
-#pragma unroll
-  for (int w = 0; w < K3_W; ++w) {
-    const int t = wsum[w];
-    before += (w < wave) ? t : 0;
-    all += t;
-  }
-  *total = all;
-  return before + x - v;
-}
 
 __global__ __launch_bounds__(K3_T) void k3_compact(int S, int k, const uint8_t* __restrict__ alive,
                                                    int32_t* __restrict__ keep, int32_t* __restrict__ kept_count,
@@ -43,46 +16,16 @@ __global__ __launch_bounds__(K3_T) void k3_compact(int S, int k, const uint8_t* 
                                                    int32_t* __restrict__ new_S) {
   __shared__ int wsum[K3_W];
   const int tid = threadIdx.x;
-  const int M = S * k;
-
-  int base = 0;
-  for (int c0 = 0; c0 < M; c0 += K3_T * K3_ITEMS) {
-    const int i0 = c0 + tid * K3_ITEMS;
-    int f[K3_ITEMS];
-    int lc = 0;
-#pragma unroll
-    for (int e = 0; e < K3_ITEMS; ++e) {
-      f[e] = (i0 + e < M) ? (alive[i0 + e] != 0) : 0;
-      lc += f[e];
-    }
-    int total;
-    int o = base + block_excl_scan(lc, wsum, &total);
-#pragma unroll
-    for (int e = 0; e < K3_ITEMS; ++e)
-      if (f[e]) keep[o++] = i0 + e;
-    base += total;
-  }
-  if (tid == 0) *kept_count = base;
+  auto is_alive = [&](int e) { return alive[e] != 0; };
+  const int kept = compact_entries_pass(S * k, is_alive, [&](int o, int e) { keep[o] = e; }, wsum);
+  if (tid == 0) *kept_count = kept;
 
   if (new_off == nullptr && kept_sent == nullptr && new_S == nullptr) return;
-  // per sentence: (survives << 20) | surviving entries, scanned together
-  int sbase = 0, ebase = 0;
-  for (int s0 = 0; s0 < S; s0 += K3_T) {
-    const int s = s0 + tid;
-    int cnt = 0;
-    if (s < S)
-      for (int j = 0; j < k; ++j) cnt += (alive[(size_t)s * k + j] != 0);
-    const int flag = cnt > 0;
-    int total;
-    const int ex = block_excl_scan(cnt | (flag << 20), wsum, &total);
-    if (flag) {
-      const int pos = sbase + (ex >> 20);
-      if (kept_sent) kept_sent[pos] = s;
-      if (new_off) new_off[pos] = ebase + (ex & 0xFFFFF);
-    }
-    sbase += total >> 20;
-    ebase += total & 0xFFFFF;
-  }
+  int sbase, ebase;
+  compact_sentences_pass(S, k, is_alive, [&](int pos, int s, int first) {
+    if (kept_sent) kept_sent[pos] = s;
+    if (new_off) new_off[pos] = first;
+  }, wsum, sbase, ebase);
   // the end of the last surviving sentence, repeated up to entry S: a launch
   // sized for more sentences than survive sees only empty ones past new_S
   if (new_off)

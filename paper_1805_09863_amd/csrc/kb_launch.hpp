@@ -8,6 +8,15 @@
 
 namespace kb {
 
+// ---------------------------------------------------------------- K1, few rows
+// Steps of at most FEW_ROWS live rows, operands 16-byte loadable: VALU
+// projection streaming W once (k1_few.hip).  Layout code K1_FEW.
+constexpr int FEW_ROWS = 8;
+constexpr int K1_FEW = 16;
+int few_chunk_words(int bf16);                   // words per chunk (one "tile")
+size_t few_lds_needed(int bf16, int N, int H);   // LDS bytes of a launch
+hipError_t launch_k1_few(int bf16, dim3 grid, const K1Args& a, hipStream_t st);
+
 // ---------------------------------------------------------------- K2
 struct K2Args {
   const float2* stats;
@@ -64,6 +73,10 @@ hipError_t launch_beam_backtrace(int S0, int k, int T, float alpha, const int32_
 // ---------------------------------------------------------------- decoder stand-in
 hipError_t launch_standin_alive(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
                                 uint8_t* alive, hipStream_t st);
+hipError_t launch_standin_step(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
+                               const float* score, int32_t* keep, int32_t* counts, int32_t* new_off,
+                               float* prev_next, int32_t* sid_next, uint8_t* alive, int32_t* counts_host,
+                               hipStream_t st);
 hipError_t launch_standin_next_h(int n_max, const int32_t* n_dev, int k, int T, int t, const int32_t* keep,
                                  const int32_t* sid, const void* table, void* out, size_t row_bytes,
                                  hipStream_t st);

@@ -5,6 +5,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 #include <string>
 
@@ -95,17 +96,39 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // Splits whose running row maxima the 256 x 256 tile kernel shares (16 keys per row).
 constexpr int kGmaxSplits = 16;
 
-// Rows from which the 256 x 256 tile pays off (it needs the DMA pipeline).
-constexpr int kWideMinRows = 513;
+// Rows from which the 256 x 256 tile pays off (it needs the DMA pipeline):
+// measured against the 128 x 256, 256 x 128 and 512 x 32 tiles at 10-1024 rows
+// (V=50k, H=1024, k=5), it is the fastest from about 130 rows (e.g. 67 against
+// 92 us at 150 rows, 103 against 147 us at 320); below, the 256-word x 128-row
+// tile wins from 65 rows and 32-row tiles below that.
+constexpr int kWideMinRows = 129;
+constexpr int kDmaL128MinRows = 65;
 // The wide kernel's W source offsets assume at least one full 256-word tile.
 constexpr int kWideMinCols = 256;
 
 // Shapes the DMA pipeline accepts, pointer alignment aside.
 bool dma_shape(int dtype, int H, int V) { return dtype == KB_BF16 && H % 128 == 0 && V % 8 == 0; }
 
-Plan make_plan(int dtype, int N, int H, int V, int k, bool dma) {
+// The few-row kernel holds every row's state in LDS next to its partial sums.
+constexpr size_t kFewLdsMax = 160 * 1024;
+// It streams W at about 4 TB/s and adds its arithmetic after the loads (about
+// 0.03-0.08 us per row and million weights), while the matrix-core kernels
+// carry about 20 us of fixed cost per step: it is the faster of the two up to
+// about 64 M row-weight products (measured on float32 and bf16 steps of 1-8
+// rows, H 256-2048, V 8k-90k).
+constexpr long long kFewMaxWork = 64ll << 20;
+
+Plan make_plan(int dtype, int N, int H, int V, int k, bool dma, bool vec) {
   Plan p{};
-  if (dma && N >= kWideMinRows && V >= kWideMinCols && dma_shape(dtype, H, V)) {
+  const int few_cw = kb::few_chunk_words(dtype == KB_BF16);
+  if (vec && N <= kb::FEW_ROWS && V >= few_cw && (long long)N * H * V <= kFewMaxWork &&
+      kb::few_lds_needed(dtype == KB_BF16, N, H) <= kFewLdsMax) {
+    // a few rows: one pass over W on the vector ALUs; chunks of few_cw words,
+    // as many splits as CUs (at most), each a run of whole chunks
+    p.layout = kb::K1_FEW;
+    p.BH = kb::FEW_ROWS;
+    p.BV = few_cw;
+  } else if (dma && N >= kWideMinRows && V >= kWideMinCols && dma_shape(dtype, H, V)) {
     p.layout = kb::K1_W256;
     p.BH = 256;
     p.BV = 256;
@@ -113,21 +136,22 @@ Plan make_plan(int dtype, int N, int H, int V, int k, bool dma) {
     p.layout = kb::K1_L256;
     p.BH = 256;
     p.BV = 128;
-  } else if (N > 32) {
+  } else if (N >= (dma ? kDmaL128MinRows : 33)) {
     p.layout = kb::K1_L128;
     p.BH = 128;
     p.BV = 256;
   } else {
-    // one row tile: the word tile sets how many CUs take part.  Of 512, 256 and
-    // 128 words, the one with the shortest split (tiles per split x (tile
-    // width + a per-tile cost of about 64 words' worth)) wins; ties keep the
-    // wider tile.
+    // 32-row tiles (one, or two on the DMA path): the word tile sets how many
+    // CUs take part.  Of 512, 256 and 128 words, the one with the shortest
+    // split (tiles per split x (tile width + a per-tile cost of about 64
+    // words' worth)) wins; ties keep the wider tile.
     static const int kLayouts[3] = {kb::K1_L32, kb::K1_L32M, kb::K1_L32S};
+    const int rt = (N + 31) / 32;
     long best = -1;
     for (int i = 0; i < 3; ++i) {
       const int bv = 512 >> i;
       const int nt = (V + bv - 1) / bv;
-      const int pp = nt < kTargetCUs ? nt : kTargetCUs;
+      const int pp = nt < kTargetCUs / rt ? nt : kTargetCUs / rt;
       const long cost = (long)((nt + pp - 1) / pp) * (bv + 64);
       if (best < 0 || cost < best) {
         best = cost;
@@ -157,8 +181,9 @@ Plan make_plan(int dtype, int N, int H, int V, int k, bool dma) {
 
 // Workspace for a shape: enough for whichever plan the pointers' alignment selects.
 size_t workspace_bytes(int dtype, int N, int H, int V, int k) {
-  const size_t a = make_plan(dtype, N, H, V, k, true).bytes, b = make_plan(dtype, N, H, V, k, false).bytes;
-  return a > b ? a : b;
+  const size_t a = make_plan(dtype, N, H, V, k, true, true).bytes, b = make_plan(dtype, N, H, V, k, false, true).bytes,
+               c = make_plan(dtype, N, H, V, k, false, false).bytes;
+  return std::max(a, std::max(b, c));
 }
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
@@ -210,8 +235,9 @@ bool vec_operands(int dtype, int H, int V, const void* h, const void* W) {
   return (H % vec == 0) && (V % vec == 0) && aligned(h, 16) && aligned(W, 16);
 }
 Plan plan_for(int dtype, int N, int H, int V, int k, const void* h, const void* W, const float* b) {
-  const bool dma = dma_shape(dtype, H, V) && vec_operands(dtype, H, V, h, W) && aligned(b, 16);
-  return make_plan(dtype, N, H, V, k, dma);
+  const bool vec = vec_operands(dtype, H, V, h, W);
+  const bool dma = dma_shape(dtype, H, V) && vec && aligned(b, 16);
+  return make_plan(dtype, N, H, V, k, dma, vec);
 }
 
 // Alignment checks, plan, threshold reset and the projection kernel (K1)
@@ -226,7 +252,7 @@ kb_status launch_projection(int dtype, int N, int H, int V, int k, const void* h
     return fail(KB_ERR_INVALID_ARG, "h, W or b misaligned for its element type");
   const bool vec_ok = vec_operands(dtype, H, V, h, W);
   const bool dma = dma_shape(dtype, H, V) && vec_ok && aligned(b, 16);
-  p = make_plan(dtype, N, H, V, k, dma);
+  p = make_plan(dtype, N, H, V, k, dma, vec_ok);
   const size_t need = workspace_bytes(dtype, N, H, V, k);
   if (!ws) return fail(KB_ERR_WORKSPACE, "workspace is null (%zu bytes needed)", need);
   if (!aligned(ws, 256)) return fail(KB_ERR_WORKSPACE, "workspace must be 256-byte aligned");
@@ -253,14 +279,20 @@ kb_status launch_projection(int dtype, int N, int H, int V, int k, const void* h
   a1.grp = p.row_tiles < 4 ? p.row_tiles : 4;
   a1.no_stats = (no_stats && p.layout == kb::K1_W256 && p.kc == 4) ? 1 : 0;
 
-  const int n_zero = p.row_tiles * p.BH * (p.layout == kb::K1_W256 ? 1 + kGmaxSplits : 1);  // gthr (+ gmax)
-  hipError_t e = kb::launch_zero_u32(a1.gthr, n_zero, hs);
-  if (e != hipSuccess) return fail(KB_ERR_HIP, "threshold reset kernel launch: %s", hipGetErrorString(e));
+  hipError_t e = hipSuccess;
+  if (p.layout != kb::K1_FEW) {  // the few-row kernel shares no thresholds
+    const int n_zero = p.row_tiles * p.BH * (p.layout == kb::K1_W256 ? 1 + kGmaxSplits : 1);  // gthr (+ gmax)
+    e = kb::launch_zero_u32(a1.gthr, n_zero, hs);
+    if (e != hipSuccess) return fail(KB_ERR_HIP, "threshold reset kernel launch: %s", hipGetErrorString(e));
+  }
   if (ev0) {
     e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev0), hs);
     if (e != hipSuccess) return fail(KB_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
   }
-  e = kb::launch_k1(dtype == KB_BF16, dma, p.layout, p.kc, dim3(p.P * p.row_tiles), a1, hs);
+  if (p.layout == kb::K1_FEW)
+    e = kb::launch_k1_few(dtype == KB_BF16, dim3(p.P), a1, hs);
+  else
+    e = kb::launch_k1(dtype == KB_BF16, dma, p.layout, p.kc, dim3(p.P * p.row_tiles), a1, hs);
   if (e != hipSuccess) return fail(KB_ERR_HIP, "projection kernel launch: %s", hipGetErrorString(e));
   if (ev1) {
     e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev1), hs);
@@ -713,6 +745,22 @@ kb_status kb_standin_alive(int S, const int32_t* S_dev, int k, int t, const int3
   hipError_t e = kb::launch_standin_alive(S, S_dev, k, t, sid, lengths, alive,
                                           reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(KB_ERR_HIP, "stand-in alive kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+kb_status kb_standin_step(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
+                          const float* score, int32_t* keep_idx, int32_t* counts, int32_t* new_sent_offsets,
+                          float* prev_next, int32_t* sid_next, uint8_t* alive, int32_t* counts_host, void* stream) {
+  if (S < 0 || k < 1) return fail(KB_ERR_INVALID_ARG, "S = %d, k = %d", S, k);
+  if ((long long)S * k > INT_MAX) return fail(KB_ERR_UNSUPPORTED, "S*k does not fit in int32");
+  if (k >= (1 << 10)) return fail(KB_ERR_UNSUPPORTED, "k = %d: at most 1023 entries per sentence", k);
+  if (!counts || !new_sent_offsets) return fail(KB_ERR_INVALID_ARG, "null counts or new_sent_offsets");
+  if (S > 0 && (!sid || !lengths || !score || !keep_idx || !prev_next || !sid_next))
+    return fail(KB_ERR_INVALID_ARG, "null sid, lengths, score, keep_idx, prev_next or sid_next");
+  hipError_t e = kb::launch_standin_step(S, S_dev, k, t, sid, lengths, score, keep_idx, counts, new_sent_offsets,
+                                         prev_next, sid_next, alive, counts_host,
+                                         reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KB_ERR_HIP, "stand-in step kernel launch: %s", hipGetErrorString(e));
   return ok();
 }
 

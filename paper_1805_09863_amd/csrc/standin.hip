@@ -7,8 +7,12 @@
 //   * standin_alive: entry s*k + r of the batch stays unless its sentence
 //     reaches its drawn length this step (every continuation ends together);
 //   * standin_next_h: the next step's state of each surviving entry, read
-//     from the table at (original sentence id, step, beam slot).
-#include "kb_launch.hpp"
+//     from the table at (original sentence id, step, beam slot);
+//   * standin_step: the mask, the compaction over it (K3's scan) and the
+//     gathers of the surviving entries' scores and sentences' ids, in one
+//     launch of one workgroup: a loop step is then the output layer, this,
+//     and the next states.
+#include "k3_scan.hpp"
 
 namespace kb {
 
@@ -38,6 +42,51 @@ __global__ __launch_bounds__(256) void standin_next_h(int n_max, const int32_t* 
     const long long src = ((long long)sid[e / k] * T + t) * k + e % k;
     out[i] = table[src * row_words + w];
   }
+}
+
+__global__ __launch_bounds__(K3_T) void standin_step(int S, const int32_t* __restrict__ S_dev, int k, int t,
+                                                     const int32_t* __restrict__ sid,
+                                                     const int32_t* __restrict__ lengths,
+                                                     const float* __restrict__ score, int32_t* __restrict__ keep,
+                                                     int32_t* __restrict__ counts, int32_t* __restrict__ new_off,
+                                                     float* __restrict__ prev_next, int32_t* __restrict__ sid_next,
+                                                     uint8_t* __restrict__ alive, int32_t* __restrict__ counts_host) {
+  __shared__ int wsum[K3_W];
+  const int tid = threadIdx.x;
+  const int live = S_dev ? min(S, *S_dev) : S;  // sentences past it do not exist this step
+  auto is_alive = [&](int e) {
+    const int s = e / k;
+    return s < live && t < lengths[sid[s]] - 1;
+  };
+  const int kept = compact_entries_pass(S * k, is_alive, [&](int o, int e) {
+    keep[o] = e;
+    prev_next[o] = score[e];
+  }, wsum);
+  int sbase, ebase;
+  compact_sentences_pass(S, k, is_alive, [&](int pos, int s, int first) {
+    new_off[pos] = first;
+    sid_next[pos] = sid[s];
+  }, wsum, sbase, ebase);
+  for (int s = sbase + tid; s <= S; s += K3_T) new_off[s] = ebase;  // empty sentences past the survivors
+  if (alive)
+    for (int e = tid; e < S * k; e += K3_T) alive[e] = is_alive(e) ? 1 : 0;
+  if (tid == 0) {
+    counts[0] = kept;
+    counts[1] = sbase;
+    if (counts_host) {  // pinned host memory: visible to the host once the kernel has completed
+      counts_host[0] = kept;
+      counts_host[1] = sbase;
+    }
+  }
+}
+
+hipError_t launch_standin_step(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
+                               const float* score, int32_t* keep, int32_t* counts, int32_t* new_off,
+                               float* prev_next, int32_t* sid_next, uint8_t* alive, int32_t* counts_host,
+                               hipStream_t st) {
+  standin_step<<<dim3(1), dim3(K3_T), 0, st>>>(S, S_dev, k, t, sid, lengths, score, keep, counts, new_off, prev_next,
+                                              sid_next, alive, counts_host);
+  return hipGetLastError();
 }
 
 hipError_t launch_standin_alive(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,

@@ -43,10 +43,10 @@ def decode_loop(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, lengths
     ``compact=False``: the batch keeps all S0 sentences until the longest is
     done (Algorithm 1); finished sentences' rows are decoded and ignored.
 
-    A compacted step enqueues the output layer, the stand-in's EOS mask, the
-    compaction, the gathers of the surviving scores and sentence ids and the
-    stand-in's next states.  The batch only shrinks, so step t + 1 is launched
-    sized by the exact counts of step t (rows, sentences), read from the
+    A compacted step enqueues the output layer, the stand-in's step (EOS
+    mask, compaction, gathers of the surviving scores and sentence ids: one
+    launch) and the stand-in's next states.  The batch only shrinks, so step
+    t + 1 is launched sized by the exact counts of step t (rows, sentences), read from the
     device while step t is still queued: the host never waits for the step it
     has just launched, and the device never waits for the host.  Every kernel
     of a step takes the exact counts of its own batch from the device (the
@@ -92,10 +92,8 @@ def decode_loop(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, lengths
     kbb.standin_next_h(h_table, ident, sid, k, T, 0, M0, out=h_cur, stream=stream)
     S, N, t = S0, M0, 0
     if compact:
-        alive = torch.empty(M0, dtype=torch.uint8, device=dev)
         keep = torch.empty(M0, **i32)
         noff = torch.empty(S0 + 1, **i32)
-        ksent = torch.empty(S0, **i32)
         # rows past a step's exact count are projected: keep them finite
         h_nx = torch.zeros((M0, H), dtype=h_table.dtype, device=dev)
         prev_nx = torch.zeros(M0, dtype=torch.float32, device=dev)
@@ -111,15 +109,12 @@ def decode_loop(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, lengths
             kbb.kbest_step(h_cur[:N], W, b, prev[:N], off[:S + 1], k, S=S,
                            out=(tok[:S * k].view(S, k), par[:S * k].view(S, k), sc[:S * k].view(S, k)),
                            ws=ws, stream=stream)
-            kbb.standin_alive(sid, lengths, S, k, t, out=alive, S_dev=S_ex, stream=stream)
-            kbb.compact_beams(alive[:S * k], S, k, out=(keep, c[0:1], noff, ksent, c[1:2]), stream=stream)
-            with torch.cuda.stream(stream):              # the copy runs on the loop's stream
-                cnt_host[t % 2].copy_(c, non_blocking=True)
+            # EOS mask, compaction, surviving scores and sentence ids: one launch
+            # (the counts also land in pinned host memory, read once the step is done)
+            kbb.standin_step(sid[:S], lengths, sc[:S * k], S, k, t,
+                             out=(keep[:S * k], c, noff[:S + 1], prev_nx[:S * k], sid_nx[:S]), S_dev=S_ex,
+                             counts_host=cnt_host[t % 2], stream=stream)
             ready[t % 2].record(stream)
-            kbb.gather_rows(sc[:S * k].view(S * k, 1), keep, n_dev=c[0:1], n_max=S * k,
-                            out=prev_nx.view(M0, 1), stream=stream)
-            kbb.gather_rows(sid[:S].view(S, 1), ksent, n_dev=c[1:2], n_max=S, out=sid_nx.view(S0, 1),
-                            stream=stream)
             if t + 1 < T:
                 kbb.standin_next_h(h_table, keep, sid, k, T, t + 1, S * k, n_dev=c[0:1], out=h_nx,
                                    stream=stream)

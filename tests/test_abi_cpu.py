@@ -51,6 +51,20 @@ def test_standin_argument_checks():
     assert nh(4, None, 5, 60, 1, FAKE, FAKE, ctypes.c_void_p(0x1002), FAKE, 2048, None) == KB_ERR_INVALID_ARG
 
 
+def test_standin_step_argument_checks():
+    L = binding.lib()
+    st = lambda *a: L.kb_standin_step(*a[:13], None, a[13])   # noqa: E731  (no host copy of the counts)
+    F = FAKE
+    assert st(-1, None, 5, 0, F, F, F, F, F, F, F, F, None, None) == KB_ERR_INVALID_ARG
+    assert st(3, None, 0, 0, F, F, F, F, F, F, F, F, None, None) == KB_ERR_INVALID_ARG
+    assert st(3, None, 1024, 0, F, F, F, F, F, F, F, F, None, None) == KB_ERR_UNSUPPORTED      # k >= 1024
+    assert st(1 << 30, None, 4, 0, F, F, F, F, F, F, F, F, None, None) == KB_ERR_UNSUPPORTED
+    for i in range(4, 12):                      # each required pointer in turn
+        args = [3, None, 5, 0] + [F] * 8 + [None, None]
+        args[i] = None
+        assert st(*args) == KB_ERR_INVALID_ARG, f"argument {i} may not be null"
+
+
 def test_abi_version_and_status_strings():
     L = binding.lib()
     assert L.kb_abi_version() == 2
@@ -249,6 +263,12 @@ def test_host_tensors_are_refused_not_computed():
         kb.compact_beams(torch.ones(10, dtype=torch.uint8), 2, 5)
     with pytest.raises(TypeError, match="on the GPU"):
         kb.compact_batch(torch.ones(10, dtype=torch.uint8))
+    with pytest.raises(TypeError, match="on the GPU"):
+        kb.binding.standin_step(torch.zeros(2, dtype=torch.int32), torch.zeros(4, dtype=torch.int32),
+                                torch.zeros(6), 2, 3, 0,
+                                out=(torch.zeros(6, dtype=torch.int32), torch.zeros(2, dtype=torch.int32),
+                                     torch.zeros(3, dtype=torch.int32), torch.zeros(6),
+                                     torch.zeros(2, dtype=torch.int32)))
 
 
 class _FakeLib:
@@ -320,6 +340,9 @@ def test_every_pointer_the_binding_passes_was_checked(monkeypatch):
     binding.standin_alive(z(S, d=i32), z(4, d=i32), S, k, 0, out=z(S * k, d=u8), S_dev=z(1, d=i32), stream=st)
     binding.standin_next_h(z(40, H, d=bf), z(S * k, d=i32), z(S, d=i32), k, 4, 1, S * k, n_dev=z(1, d=i32),
                            out=z(S * k, H, d=bf), stream=st)
+    binding.standin_step(z(S, d=i32), z(4, d=i32), z(S * k), S, k, 0,
+                         out=(z(S * k, d=i32), z(2, d=i32), z(S + 1, d=i32), z(S * k), z(S, d=i32)),
+                         S_dev=z(1, d=i32), alive=z(S * k, d=u8), stream=st)
     fin = (z(4, d=i32), z(4 * k), z(4 * k, d=i32), z(4 * k, d=i32))
     binding.beam_finish(S, k, 0, 4, 1, out3[0], out3[1], out3[2], z(S, d=i32), z(S, d=i32), z(S, d=i32), 0, 0,
                         z(4 * S * k, d=i32), z(4 * S * k, d=i32), fin, z(S * k, d=u8), stream=st)

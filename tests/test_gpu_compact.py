@@ -109,6 +109,53 @@ def test_standin_alive_device_count(kb, S_live):
     assert np.array_equal(alive.cpu().numpy(), want)
 
 
+@pytest.mark.parametrize("S,k,S_live", [(0, 5, None), (20, 3, None), (20, 3, 0), (20, 3, 9), (1, 5, None), (512, 5, 300),
+                                         (1500, 4, 1400), (2048, 12, None)])
+def test_standin_step_matches_its_definition(kb, S, k, S_live):
+    # the fused step = the stand-in's EOS mask, the stable compaction of that
+    # mask (np.flatnonzero), the sentence offsets and the two gathers; sentences
+    # past the device count are dropped without reading their (stale) ids
+    from paper_1805_09863_amd import binding as kbb
+    g = np.random.default_rng(S * 7 + k)
+    t = 6
+    n_orig = S + 40
+    lengths = g.integers(1, 14, n_orig).astype(np.int32)
+    lengths[n_orig - 1] = 13                      # the stale id below: would read as alive
+    sid = g.permutation(n_orig - 1)[:S].astype(np.int32)
+    live = S if S_live is None else min(S, S_live)
+    score = g.standard_normal(S * k).astype(np.float32)
+    mask = np.repeat((np.arange(S) < live) & (t < lengths[np.where(np.arange(S) < live, sid, 0)] - 1), k)
+    keep_want = np.flatnonzero(mask).astype(np.int32)
+    sent_alive = mask.reshape(S, k).any(axis=1)
+    ks = np.flatnonzero(sent_alive)
+    per_sent = mask.reshape(S, k).sum(axis=1)[ks]
+    off_want = np.concatenate([[0], np.cumsum(per_sent)]).astype(np.int32)
+    sid_dev = torch.from_numpy(sid).cuda()
+    sid_dev[live:] = n_orig - 1                   # stale ids past the device count
+    keep = torch.full((S * k,), -9, dtype=torch.int32, device="cuda")
+    counts = torch.full((2,), -9, dtype=torch.int32, device="cuda")
+    noff = torch.full((S + 1,), -9, dtype=torch.int32, device="cuda")
+    prev_next = torch.full((S * k,), float("nan"), dtype=torch.float32, device="cuda")
+    sid_next = torch.full((S,), -9, dtype=torch.int32, device="cuda")
+    alive = torch.full((S * k,), 7, dtype=torch.uint8, device="cuda")
+    s_dev = None if S_live is None else torch.tensor([S_live], dtype=torch.int32, device="cuda")
+    counts_host = torch.full((2,), -9, dtype=torch.int32, pin_memory=True)
+    kbb.standin_step(sid_dev, torch.from_numpy(lengths).cuda(), torch.from_numpy(score).cuda(), S, k, t,
+                     out=(keep, counts, noff, prev_next, sid_next), S_dev=s_dev, alive=alive,
+                     counts_host=counts_host)
+    torch.cuda.synchronize()
+    n, ns = (int(x) for x in counts.cpu())
+    assert counts_host.tolist() == [n, ns]        # the copy the kernel writes to pinned host memory
+    assert (n, ns) == (keep_want.size, ks.size)
+    assert np.array_equal(keep.cpu().numpy()[:n], keep_want)
+    assert np.array_equal(alive.cpu().numpy(), mask.astype(np.uint8))
+    noff_h = noff.cpu().numpy()
+    assert np.array_equal(noff_h[:ns + 1], off_want)
+    assert (noff_h[ns:] == n).all()               # empty sentences past the survivors
+    assert np.array_equal(prev_next.cpu().numpy()[:n].view(np.uint32), score[keep_want].view(np.uint32))
+    assert np.array_equal(sid_next.cpu().numpy()[:ns], sid[ks])
+
+
 # ---------------------------------------------------------------- the M-entry form (kb_compact_batch)
 def _entries(M, g, max_sent=6):
     sizes = g.integers(0, max_sent + 1, M + 1)                # empty sentences included

@@ -46,6 +46,9 @@ SMALL = [
     ([4, 4], 64, 40000, 3, "f32"),             # 256-word tiles, register-staged f32
     ([16, 16], 128, 70000, 16, "bf16"),        # 512-word tiles, k = 16, 32 rows
     ([2, 3, 1], 128, 20000, 2, "bf16"),        # k = 2: merge lanes staged in pairs
+    ([10] * 5, 128, 20000, 6, "bf16"),         # 50 rows: two 32-row tiles, DMA pipeline
+    ([16] * 4, 256, 30000, 16, "bf16"),        # 64 rows: two full 32-row tiles, k = 16
+    ([13] * 7, 128, 8000, 5, "bf16"),          # 91 rows: one 128-row tile, DMA pipeline
 ]
 
 
@@ -60,10 +63,14 @@ def test_small_shapes(kb, case):
 
 
 # Shapes for the 256 x 256-tile projection kernel (bf16, H % 128 == 0,
-# V % 8 == 0, at least 513 rows): ragged last row and word tiles, a last
+# V % 8 == 0, at least 129 rows): ragged last row and word tiles, a last
 # word tile holding only 8 words, the shortest state (4 stages per tile),
-# one tile per split, k = 1 and k = 16.
+# one tile per split, k = 1 and k = 16, a single row tile mostly padding.
 WIDE = [
+    ([1] * 129, 128, 3000, 1),                 # the fewest rows it takes: 127 padding rows
+    ([5] * 40, 256, 9000, 5),                  # N 200
+    ([12] * 25 + [7], 128, 5000, 12),          # N 307: two row tiles, the second ragged
+    ([4] * 128, 1024, 50000, 4),               # N 512: two whole row tiles
     ([5] * 120, 128, 2056, 5),                 # N 600; last word tile holds 8 words
     ([12] * 50, 256, 5000, 12),                # N 600; ragged word tile of 136
     ([16] * 40, 384, 3000, 16),                # k = 16, 12 stages per tile
@@ -237,7 +244,7 @@ def _poisoned_run(kb, dev_in, inp, ws_byte, out_fill):
 
 @pytest.mark.parametrize("which", ["v90k", "flat_bias_1280"])
 def test_wide_kernel_deterministic_with_poisoned_buffers(kb, which):
-    # the 256 x 256 projection kernel (N >= 513) run twice: outputs pre-filled
+    # the 256 x 256 projection kernel (N >= 129) run twice: outputs pre-filled
     # with -7 / NaN and with 7 / -inf, the workspace with 0xFF and with 0x7F.
     # Shared thresholds arrive at timing-dependent moments; the results must
     # not depend on them, bit for bit
