@@ -126,15 +126,22 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ void atomic_umax_nowait(uint32_t* p, uint32_t v) {
   asm volatile("global_atomic_umax %0, %1, off" ::"v"(p), "v"(v) : "memory");
 }
-__device__ __forceinline__ u32x4 load16_async(const void* p) {
-  u32x4 v;
-  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(p));
+// 4-byte load from a wave-uniform base (SGPR pair) plus a per-lane byte offset
+__device__ __forceinline__ uint32_t load4_async(uint32_t voff, const void* sbase) {
+  const uint64_t p = reinterpret_cast<uint64_t>(sbase);
+  const uint64_t u = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(p >> 32)) << 32) |
+                     (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)p);
+  uint32_t v;
+  asm volatile("global_load_dword %0, %1, %2" : "=v"(v) : "v"(voff), "s"(reinterpret_cast<const void*>(u)));
   return v;
 }
 // every vector memory operation of the wave done; the registers pass
 // through so that their uses stay behind the wait
-__device__ __forceinline__ void load_wait(u32x4& a, u32x4& b, u32x4& c, u32x4& d) {
-  asm volatile("s_waitcnt vmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d));
+__device__ __forceinline__ void load_wait(uint32_t (&v)[16]) {
+  asm volatile("s_waitcnt vmcnt(0)"
+               : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]), "+v"(v[7]),
+                 "+v"(v[8]), "+v"(v[9]), "+v"(v[10]), "+v"(v[11]), "+v"(v[12]), "+v"(v[13]), "+v"(v[14]),
+                 "+v"(v[15]));
 }
 
 __device__ __forceinline__ float max4(const f32x16& x, int q) {
@@ -363,12 +370,13 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
     const int par = ti & 1;
     const int v0 = (split + ti * a.P) * BV;
     // the running maxima splits 0..MS-1 have shared for the owner's row
-    // (loaded now, used after the statistics)
-    u32x4 gm[4];
+    // (loaded now, used after the statistics; split-major, so each load of
+    // the wave reads 64 consecutive rows)
+    uint32_t key[G::MS];
     if (kShare && ti > 0) {
-      const uint32_t* gp = a.gmax + (size_t)(h0 + tid) * G::MS;
+      const size_t stride = (size_t)a.row_tiles * BH;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) gm[i] = load16_async(gp + 4 * i);
+      for (int i = 0; i < G::MS; ++i) key[i] = load4_async(4u * tid, a.gmax + h0 + i * stride);
     }
     float tmax[4];
     // statistics (Algorithm 4, one rescale per tile)
@@ -412,15 +420,7 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
       // is worked out only where at least k of them beat the row's present
       // threshold (else it cannot raise it): insertion into a right-aligned
       // descending list by median-of-three.
-      load_wait(gm[0], gm[1], gm[2], gm[3]);  // long landed: issued before the statistics
-      uint32_t key[G::MS];
-#pragma unroll
-      for (int i = 0; i < G::MS / 4; ++i) {
-        key[4 * i] = gm[i].x;
-        key[4 * i + 1] = gm[i].y;
-        key[4 * i + 2] = gm[i].z;
-        key[4 * i + 3] = gm[i].w;
-      }
+      load_wait(key);  // long landed: issued before the statistics
       const uint32_t tk = max(f2key(ep.thr[tid]), ep.tgk[par][tid]);
       int above = 0;
 #pragma unroll
@@ -604,7 +604,7 @@ __global__ __launch_bounds__(256, 1) void k1_wide(K1Args a) {
     // score of the split is a valid entry of the shared maxima)
     if ((ti & (ti - 1)) == 0) publish(ep.thr[tid]);
     if (kShare && split < G::MS && (ti & (ti - 1)) == 0 && rowbest > shared_best && h0 + tid < a.N) {
-      atomic_umax_nowait(&a.gmax[(size_t)(h0 + tid) * G::MS + split], f2key(rowbest));
+      atomic_umax_nowait(&a.gmax[(size_t)split * a.row_tiles * BH + h0 + tid], f2key(rowbest));
       shared_best = rowbest;
     }
   };

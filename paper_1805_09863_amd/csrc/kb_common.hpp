@@ -60,7 +60,8 @@ struct K1Args {
   float2* stats;      // [P][N]   (max, sum of exp(x - max)) of each split
   int2* lists;        // [P][N][k] (score bits, word) of each split, best first
   uint32_t* gthr;     // [row_tiles * BH] shared per-row threshold keys (order-preserving), zeroed per call
-  uint32_t* gmax;     // [row_tiles * BH][16] running-max keys of splits 0..15 per row, zeroed per call
+  uint32_t* gmax;     // [16][row_tiles * BH] running-max keys of splits 0..15 per row (split-major:
+                      // a wave's updates and reads touch 64 consecutive rows), zeroed per call
                       // (256 x 256 tile kernel only)
   int row_tiles;      // R
   int P;              // vocabulary splits
