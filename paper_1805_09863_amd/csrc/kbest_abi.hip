@@ -132,11 +132,13 @@ Plan make_plan(int dtype, int N, int H, int V, int k, bool dma, bool vec) {
     p.layout = kb::K1_W256;
     p.BH = 256;
     p.BV = 256;
-  } else if (N > 192) {
+  } else if (N > 192 && dtype == KB_BF16) {
     p.layout = kb::K1_L256;
     p.BH = 256;
     p.BV = 128;
   } else if (N >= (dma ? kDmaL128MinRows : 33)) {
+    // (float32 keeps this tile at every size: 9-10% faster than 128 words x
+    // 256 rows from 320 to 2048 rows, H=512, V=30k)
     p.layout = kb::K1_L128;
     p.BH = 128;
     p.BV = 256;
