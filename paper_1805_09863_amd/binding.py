@@ -94,9 +94,18 @@ def _ptr_host(t: Optional[torch.Tensor]):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
-def _stream(stream) -> ctypes.c_void_p:
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
+def _stream(stream, device: Optional[torch.device] = None) -> ctypes.c_void_p:
+    """The hipStream_t to launch on: ``stream``'s, else the current stream of
+    ``device`` (by default the current device), read as a raw handle without
+    building a torch.cuda.Stream object."""
     if stream is None:
-        stream = torch.cuda.current_stream()
+        if _raw_stream is not None:
+            idx = device.index if device is not None and device.index is not None else torch.cuda.current_device()
+            return ctypes.c_void_p(_raw_stream(idx))
+        stream = torch.cuda.current_stream(device)
     return ctypes.c_void_p(stream.cuda_stream)
 
 
@@ -192,7 +201,7 @@ def kbest_step(h: torch.Tensor, W: torch.Tensor, b: torch.Tensor, prev_score: to
     L = lib()
     args = [dt, N, H, V, k, S, _ptr(h), _ptr(W), _ptr(b), _ptr(prev_score), _ptr(sent_offsets),
             _ptr(tok), _ptr(par), _ptr(sc), _ptr(row_lse), _ptr(ws), ws.numel() * ws.element_size(),
-            _stream(stream)]
+            _stream(stream, dev)]
     if events is None:
         _check(L.kb_kbest_step(*args))
     else:

@@ -3,14 +3,14 @@
 // One workgroup per sentence, W waves (one per row of an average sentence,
 // W <= 16, and no more than the staged lists fit in LDS); the sentence's rows
 // are taken W at a time, one per wave:
-//   * the row's P split lists are staged in LDS, eight loads in flight per
-//     lane, and its P split statistics held in registers;
+//   * the row's P split lists are staged in LDS, eight or sixteen loads in
+//     flight per lane, and its P split statistics held in registers;
 //   * LSE = M + ln(sum_p s_p * exp(m_p - M)) over the P split partials -- the
 //     rescaling identity of Algorithm 4 applied between shards, the reduction
 //     step of Algorithm 6 extended from (max, best) to softmax statistics;
-//   * the row's best words: rounds of a wave-wide arg-best (DPP) over the
-//     heads of the P sorted split lists (strict total order: higher score,
-//     then lower word).  Each lane keeps its lists' heads and the entries
+//   * the row's best words: rounds of a wave-wide maximum of 64-bit keys
+//     (wave_keys.hpp) over the heads of the P sorted split lists (strict
+//     total order: higher score, then lower word).  Each lane keeps its lists' heads and the entries
 //     after them in registers, so a round reads no LDS on its critical path.
 //     The rounds stop once a score (prev + x - LSE) falls below the sentence's
 //     k-th best so far: the row's later entries are worse still;
@@ -21,6 +21,7 @@
 //     best lie in the union of its rows' k best, so nothing outside these
 //     candidates can be selected.
 #include "kb_launch.hpp"
+#include "wave_keys.hpp"
 
 namespace kb {
 
@@ -37,10 +38,6 @@ static_assert(K2_C % 2 == 0, "candidate keys are read in pairs");
 template <int CTRL>
 __device__ __forceinline__ float dpp_f(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
-}
-template <int CTRL>
-__device__ __forceinline__ int dpp_i(int v) {
-  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
 }
 constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
 __device__ __forceinline__ float lane_f(float v, int l) {
@@ -61,49 +58,9 @@ __device__ __forceinline__ float wave_sum(float v) {
   v += dpp_f<kDppMirror>(v);
   return (lane_f(v, 0) + lane_f(v, 16)) + (lane_f(v, 32) + lane_f(v, 48));
 }
-// the best (score, word) of the wave under better(); every lane gets it
-template <int CTRL>
-__device__ __forceinline__ void argbest_step(float& v, int& i) {
-  const float ov = dpp_f<CTRL>(v);
-  const int oi = dpp_i<CTRL>(i);
-  if (better(ov, oi, v, i)) {
-    v = ov;
-    i = oi;
-  }
-}
-__device__ __forceinline__ void wave_argbest(float& v, int& i) {
-  argbest_step<kDppXor1>(v, i);
-  argbest_step<kDppXor2>(v, i);
-  argbest_step<kDppHalfMirror>(v, i);
-  argbest_step<kDppMirror>(v, i);
-  float bv = lane_f(v, 0);
-  int bi = __builtin_amdgcn_readlane(i, 0);
-#pragma unroll
-  for (int l = 16; l < 64; l += 16) {
-    const float ov = lane_f(v, l);
-    const int oi = __builtin_amdgcn_readlane(i, l);
-    if (better(ov, oi, bv, bi)) {
-      bv = ov;
-      bi = oi;
-    }
-  }
-  v = bv;
-  i = bi;
-}
-
-// A candidate as one 64-bit key whose unsigned order is the merge order:
-// the score mapped to an order-preserving integer (-0 taken as +0, as the
-// float comparison does) above the complement of the flat index, so a higher
-// score, then a lower flat index, gives the larger key.
-__device__ __forceinline__ uint64_t cand_key(float score, int flat) {
-  const uint32_t u = (uint32_t)__float_as_int(score + 0.f);
-  const uint32_t o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-  return ((uint64_t)o << 32) | (uint32_t)~(uint32_t)flat;
-}
-__device__ __forceinline__ float key_score(uint64_t key) {
-  const uint32_t o = (uint32_t)(key >> 32);
-  return __int_as_float((int)((o & 0x80000000u) ? (o & 0x7fffffffu) : ~o));
-}
+// A candidate of the sentence merge as one 64-bit key (key_of) of its score
+// and flat index: a higher score, then a lower flat index, gives the larger key.
+__device__ __forceinline__ uint64_t cand_key(float score, int flat) { return key_of(score, flat); }
 
 template <int NQ>  // split lists per lane: P <= 64 * NQ
 __global__ __launch_bounds__(1024) void k2_merge(K2Args a) {
@@ -143,32 +100,39 @@ __global__ __launch_bounds__(1024) void k2_merge(K2Args a) {
     const bool active = ri < nrows;
     const int r = cr0 + ri;
     float2 st[NQ];
+    float prev_r = 0.f;
     if (active) {
+      // the row's split statistics and previous score first, so that their
+      // loads are in flight with the lists' (one memory round trip for a
+      // row whose lists take one batch)
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int p = lane + 64 * q;
+        st[q] = p < P ? a.stats[(size_t)p * a.N + r] : make_float2(kStatInit, 0.f);
+      }
+      prev_r = a.prev[r];
       // lane = kp * g + j (kp: k rounded up to a power of two) stages entry j
       // of lists p0 + g, p0 + gpl + g, ... (gpl = 64 / kp lists per load;
-      // slots k .. kp - 1 get empty entries): eight loads in flight per lane
-      // before the first LDS write.  Slots past kp are never read before a
-      // list has given up all k entries, so they stay unwritten.
+      // slots k .. kp - 1 get empty entries): LB loads in flight per lane
+      // before the first LDS write (16 while the registers allow, 8 for the
+      // longest split counts).  Slots past kp are never read before a list
+      // has given up all k entries, so they stay unwritten.
+      constexpr int LB = NQ <= 2 ? 16 : 8;
       const int lgk = k <= 1 ? 0 : (k <= 2 ? 1 : (k <= 4 ? 2 : (k <= 8 ? 3 : 4)));
       const int j = lane & ((1 << lgk) - 1), g = lane >> lgk, gpl = 64 >> lgk;
-      for (int p0 = 0; p0 < P; p0 += 8 * gpl) {
-        int2 v[8];
+      for (int p0 = 0; p0 < P; p0 += LB * gpl) {
+        int2 v[LB];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < LB; ++u) {
           const int p = p0 + u * gpl + g;
           v[u] = make_int2(kNegInfBits, INT_MAX);
           if (p < P && j < k) v[u] = a.lists[((size_t)p * a.N + r) * k + j];
         }
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < LB; ++u) {
           const int p = p0 + u * gpl + g;
           if (p < P) lists_dyn[wbase + p * K2_LS + j] = v[u];
         }
-      }
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        const int p = lane + 64 * q;
-        st[q] = p < P ? a.stats[(size_t)p * a.N + r] : make_float2(kStatInit, 0.f);
       }
     }
     __syncthreads();  // the staged lists are visible; the running best is settled
@@ -185,35 +149,28 @@ __global__ __launch_bounds__(1024) void k2_merge(K2Args a) {
       S = wave_sum(S);
       const float lse = M + __logf(S);
       if (a.row_lse != nullptr && lane == 0) a.row_lse[r] = lse;
-      const float base = a.prev[r] - lse;
+      const float base = prev_r - lse;
       const float kth = key_score(key[k - 1]);  // running k-th best (-inf before the first chunk)
 
-      // per list of this lane: the head (entry ptr) and the entry after it
-      float hv[NQ], nv[NQ];
-      int hi[NQ], ni[NQ], ptr[NQ];
+      // per list of this lane: the key of its head (entry ptr) and the entry after it
+      uint64_t hk[NQ];
+      int2 nx[NQ];
+      int ptr[NQ];
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
         const int2 h = lists_dyn[lidx[q]];
-        const int2 n = lists_dyn[lidx[q] + 1];
-        hv[q] = __int_as_float(h.x);
-        hi[q] = h.y;
-        nv[q] = __int_as_float(n.x);
-        ni[q] = n.y;
+        nx[q] = lists_dyn[lidx[q] + 1];
+        hk[q] = key_of(__int_as_float(h.x), h.y);
         ptr[q] = 0;
       }
       for (int jr = 0; jr < k; ++jr) {
-        float bv = -INFINITY;
-        int bi = INT_MAX, bq = -1;
+        // the wave-wide best head (branch-free: DPP and scalar maxima on keys)
+        uint64_t best = hk[0];
 #pragma unroll
-        for (int q = 0; q < NQ; ++q)
-          if (better(hv[q], hi[q], bv, bi)) {
-            bv = hv[q];
-            bi = hi[q];
-            bq = q;
-          }
-        float wv = bv;
-        int wi = bi;
-        wave_argbest(wv, wi);
+        for (int q = 1; q < NQ; ++q) best = hk[q] > best ? hk[q] : best;
+        const uint64_t win = wave_max64(best);
+        const float wv = key_score(win);
+        const int wi = key_index(win);
         // the row's later entries are worse still: once this one scores below
         // the sentence's k-th best of the rows ranked so far, none can enter
         if (wv + base < kth) break;
@@ -221,20 +178,18 @@ __global__ __launch_bounds__(1024) void k2_merge(K2Args a) {
           my_key = cand_key(wv + base, (r - r0) * a.V + wi);
           my_t = wi;
         }
-        // the lane whose head won advances that list (entries are unique);
-        // every lane then reloads the entry after its head, so the read is
-        // waited for only at the next advance.  A list advances at most k
-        // times, and its head is compared only while rounds remain, so the
-        // clamped read past the last slot is never used.
+        // the list whose head won advances (words are unique; empty heads
+        // are all alike and advance together); every lane then reloads the
+        // entry after its heads, so the read is waited for only at the next
+        // advance.  A list advances at most once a round, k rounds in all,
+        // and its head is compared only while rounds remain, so the clamped
+        // read past the last slot is never used.
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
-          const bool adv = bq == q && bv == wv && bi == wi;
-          hv[q] = adv ? nv[q] : hv[q];
-          hi[q] = adv ? ni[q] : hi[q];
+          const bool adv = hk[q] == win;
+          hk[q] = adv ? key_of(__int_as_float(nx[q].x), nx[q].y) : hk[q];
           ptr[q] += adv ? 1 : 0;
-          const int2 n = lists_dyn[lidx[q] + min(ptr[q] + 1, K2_LS - 1)];
-          nv[q] = __int_as_float(n.x);
-          ni[q] = n.y;
+          nx[q] = lists_dyn[lidx[q] + min(ptr[q] + 1, K2_LS - 1)];
         }
       }
     }
@@ -292,7 +247,7 @@ hipError_t launch_zero_u32(uint32_t* p, int n, hipStream_t st) {
 // Greedy (beam 1) merge, the reduction of Algorithm 6: per row, the best
 // (score, word) over the P split lists of length 1, in the strict order
 // higher score, then lower word.  One wave per row: each lane scans the
-// splits lane, lane + 64, ..., then a wave-wide arg-best.  Empty list slots
+// splits lane, lane + 64, ..., then the wave-wide largest key.  Empty list slots
 // hold scores below every real one, and the split holding the row's maximum
 // always lists it.
 __global__ __launch_bounds__(256) void k2_argmax(const int2* __restrict__ lists, int P, int N,
@@ -300,20 +255,16 @@ __global__ __launch_bounds__(256) void k2_argmax(const int2* __restrict__ lists,
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (r >= N) return;  // whole waves leave together
-  float bv = -INFINITY;
-  int bi = INT_MAX;
+  uint64_t best = kEmptyKey;
   for (int p = lane; p < P; p += 64) {
     const int2 e = lists[(size_t)p * N + r];
-    const float v = __int_as_float(e.x);
-    if (better(v, e.y, bv, bi)) {
-      bv = v;
-      bi = e.y;
-    }
+    const uint64_t key = key_of(__int_as_float(e.x), e.y);
+    best = key > best ? key : best;
   }
-  wave_argbest(bv, bi);
+  best = wave_max64(best);
   if (lane == 0) {
-    tok[r] = bi;
-    val[r] = bv;
+    tok[r] = key_index(best);
+    val[r] = key_score(best);
   }
 }
 
@@ -332,10 +283,13 @@ static hipError_t launch_k2_nq(const K2Args& a, hipStream_t st) {
   const int rows_per = (a.N + a.S - 1) / a.S;
   const int W = (int)std::min<size_t>(std::min(K2_MAXW, std::max(1, rows_per)), (144 * 1024) / per_wave);
   const size_t lds = (size_t)K2_LS * sizeof(int2) + (size_t)W * per_wave;
-  if (lds > 48 * 1024) {
+  static bool attr_set = false;  // the kernel's LDS ceiling (at most 144 KB + one list), raised once per process
+  if (lds > 48 * 1024 && !attr_set) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k2_merge<NQ>),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+                                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             (int)(K2_LS * sizeof(int2) + 144 * 1024));
     if (e != hipSuccess) return e;
+    attr_set = true;
   }
   k2_merge<NQ><<<dim3(a.S), dim3(64 * W), lds, st>>>(a);
   return hipGetLastError();

@@ -14,7 +14,7 @@ namespace kb {
 constexpr int FEW_ROWS = 8;
 constexpr int K1_FEW = 16;
 int few_chunk_words(int bf16);                   // words per chunk (one "tile")
-size_t few_lds_needed(int bf16, int N, int H);   // LDS bytes of a launch
+size_t few_lds_needed(int bf16, int N, int H, int tps);  // LDS bytes of a launch (tps chunks per split)
 hipError_t launch_k1_few(int bf16, dim3 grid, const K1Args& a, hipStream_t st);
 
 // ---------------------------------------------------------------- K2

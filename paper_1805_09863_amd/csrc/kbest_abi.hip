@@ -121,8 +121,9 @@ constexpr long long kFewMaxWork = 64ll << 20;
 Plan make_plan(int dtype, int N, int H, int V, int k, bool dma, bool vec) {
   Plan p{};
   const int few_cw = kb::few_chunk_words(dtype == KB_BF16);
+  const int few_nt = (V + few_cw - 1) / few_cw, few_p = std::min(few_nt, kTargetCUs);
   if (vec && N <= kb::FEW_ROWS && V >= few_cw && (long long)N * H * V <= kFewMaxWork &&
-      kb::few_lds_needed(dtype == KB_BF16, N, H) <= kFewLdsMax) {
+      kb::few_lds_needed(dtype == KB_BF16, N, H, (few_nt + few_p - 1) / few_p) <= kFewLdsMax) {
     // a few rows: one pass over W on the vector ALUs; chunks of few_cw words,
     // as many splits as CUs (at most), each a run of whole chunks
     p.layout = kb::K1_FEW;
