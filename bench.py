@@ -288,7 +288,9 @@ PEAK_F32_TFLOPS = 157.3
 
 def configs_bench(torch, np, kb, reps: int = 50):
     """Every single-step workload (the decode-loop one is timed by the loop):
-    warm steps back to back (median and min of per-step HIP events), cold steps
+    warm steps back to back (HIP events around all of them: the time per
+    step), each step alone between its own events (latency: median and min;
+    an event record costs the device a few microseconds), cold steps
     after a 512 MB write, the projection kernel alone, its roofline, and the
     fp64 oracle on the whole workload beside it (on the host's cores)."""
     from oracle import kbest_oracle as ko
@@ -313,7 +315,13 @@ def configs_bench(torch, np, kb, reps: int = 50):
             step()
         torch.cuda.synchronize()
         pairs = [(ev.create(), ev.create()) for _ in range(reps)]
-        for i in range(reps):              # warm: per-step events around the whole call
+        ev.record(pairs[0][0], stream)     # warm, back to back: one pair of events around all the steps
+        for i in range(reps):
+            step()
+        ev.record(pairs[0][1], stream)
+        torch.cuda.synchronize()
+        b2b = ev.elapsed_ms(*pairs[0]) / reps
+        for i in range(reps):              # warm latency: each step alone between its own events
             ev.record(pairs[i][0], stream)
             step()
             ev.record(pairs[i][1], stream)
@@ -352,12 +360,13 @@ def configs_bench(torch, np, kb, reps: int = 50):
             ko.kbest_step(inp.h, inp.W, inp.b, inp.prev, inp.off, k, dtype=inp.dtype)
         orc = (time.perf_counter() - t0) / orc_runs if whole else None
         res.append({"workload": inp.name, "N": N, "H": H, "V": V, "k": k, "dtype": inp.dtype,
-                    "step_ms_median": warm[len(warm) // 2], "step_ms_min": warm[0],
+                    "step_ms": b2b, "step_latency_ms_median": warm[len(warm) // 2],
+                    "step_latency_ms_min": warm[0],
                     "cold_step_ms_median": cold[len(cold) // 2], "kernel_ms_median": km,
-                    "hyps_per_s": N / (warm[len(warm) // 2] * 1e-3), "roofline": roof,
+                    "hyps_per_s": N / (b2b * 1e-3), "roofline": roof,
                     "oracle_s": orc, "oracle_hyps_per_s": (N / orc) if orc else None})
-        log(f"{inp.name}: step {warm[len(warm) // 2]:.4f} ms, kernel {km:.4f} ms, {roof['bound']} "
-            f"{roof['frac'] * 100:.1f}%, oracle {orc}")
+        log(f"{inp.name}: step {b2b:.4f} ms back to back, {warm[len(warm) // 2]:.4f} ms alone, kernel {km:.4f} ms, "
+            f"{roof['bound']} {roof['frac'] * 100:.1f}%, oracle {orc}")
     del flush
     return res
 

@@ -42,8 +42,10 @@ kb_status kb_standin_alive(int S, const int32_t* S_dev, int k, int t, const int3
  * kb_standin_step -- the bookkeeping of one loop step after the output layer,
  * in one launch: the mask of kb_standin_alive, the compaction of
  * kb_compact_beams over it (the same scan: Section 2.1, Algorithm 2's removal
- * of finished hypotheses, stable), and the gathers that carry the surviving
- * entries' scores and the surviving sentences' original ids to the next step.
+ * of finished hypotheses, stable), the gathers that carry the surviving
+ * entries' scores and the surviving sentences' original ids to the next
+ * step, and, if next_h is given, the gather of kb_standin_next_h for step
+ * t + 1 (the surviving entries' next states).
  *   S, S_dev, k, t, sid, lengths   as kb_standin_alive (sid is read only for
  *              sentences below min(S, *S_dev)).
  *   score      S*k float32, the step's scores (kb_kbest_step's out_score).
@@ -54,19 +56,29 @@ kb_status kb_standin_alive(int S, const int32_t* S_dev, int k, int t, const int3
  *   prev_next  S*k float32 out: prev_next[i] = score[keep_idx[i]], i < counts[0].
  *   sid_next   S int32 out: the original id of surviving sentence j, j < counts[1].
  *   alive      NULL or S*k uint8 out: the mask itself.
- *   counts_host  NULL or 2 int32 of pinned host memory (allocated pinned, so
- *              the device can write it): the counts again, for a host that
- *              reads them once the step's work has completed (an event on
- *              `stream`), without a separate copy.
+ *   counts_host  NULL or 3 int32 of pinned host memory (allocated pinned, so
+ *              the device can write it): [0], [1] the counts again, then
+ *              [2] = t + 1, each after a system-scope fence: a host that
+ *              polls [2] for t + 1 (having set it to another value first)
+ *              reads the counts without an event or a separate copy.
+ *   table, T, next_h, row_bytes   NULL next_h: no state gather (table, T and
+ *              row_bytes are not read).  Else as kb_standin_next_h with
+ *              step t + 1, keep = keep_idx and n = counts[0]: row i of next_h
+ *              (i < counts[0]) = table row ((sid[e/k] * T + t + 1) * k + e%k),
+ *              e = keep_idx[i]; next_h holds S*k rows of row_bytes; requires
+ *              t + 1 < T, row_bytes a positive multiple of 4, table and
+ *              next_h 4-byte aligned.  Rows past counts[0] are not written.
  * Buffers are distinct, caller-owned device memory (counts_host aside).  S == 0 writes counts = 0
- * and new_sent_offsets[0] = 0.  1 <= k < 1024; S*k fits in int32.  One
- * workgroup does it all (the batches of a decode loop are a few thousand
- * entries).  KB_ERR_INVALID_ARG for null required pointers or bad sizes.
+ * and new_sent_offsets[0] = 0.  1 <= k < 1024; S*k fits in int32.  Workgroup
+ * 0 does the bookkeeping; with next_h every workgroup (one per 32 KB of
+ * states) also works the compaction out in its own LDS and gathers its share
+ * of the states, so the whole step is one launch up to 16384 entries (two
+ * launches above).  KB_ERR_INVALID_ARG for null required pointers or bad sizes.
  */
 kb_status kb_standin_step(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
                           const float* score, int32_t* keep_idx, int32_t* counts, int32_t* new_sent_offsets,
                           float* prev_next, int32_t* sid_next, uint8_t* alive, int32_t* counts_host,
-                          void* stream);
+                          const void* table, int T, void* next_h, size_t row_bytes, void* stream);
 
 /*
  * kb_standin_next_h -- the states of step t for the entries kept by

@@ -54,7 +54,7 @@ SIGNATURES = {
     # decoder stand-in of the synthetic decode loop (include/kbest_standin.h)
     "kb_standin_alive": (_I, [_I, _P, _I, _I, _P, _P, _P, _P]),
     "kb_standin_next_h": (_I, [_I, _P, _I, _I, _I, _P, _P, _P, _P, _SZ, _P]),
-    "kb_standin_step": (_I, [_I, _P, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "kb_standin_step": (_I, [_I, _P, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _P, _SZ, _P]),
 }
 
 
@@ -86,27 +86,29 @@ def _check(status: int):
 
 
 def _ptr(t: Optional[torch.Tensor]):
-    return None if t is None else ctypes.c_void_p(t.data_ptr())
+    # a plain int: the declared argtypes (c_void_p) convert it, at a fraction
+    # of the cost of building a c_void_p per pointer
+    return None if t is None else t.data_ptr()
 
 
 def _ptr_host(t: Optional[torch.Tensor]):
     """Address of a pinned host tensor (checked by the caller) that kernels write."""
-    return None if t is None else ctypes.c_void_p(t.data_ptr())
+    return None if t is None else t.data_ptr()
 
 
 _raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
 
 
-def _stream(stream, device: Optional[torch.device] = None) -> ctypes.c_void_p:
+def _stream(stream, device: Optional[torch.device] = None) -> int:
     """The hipStream_t to launch on: ``stream``'s, else the current stream of
     ``device`` (by default the current device), read as a raw handle without
     building a torch.cuda.Stream object."""
     if stream is None:
         if _raw_stream is not None:
             idx = device.index if device is not None and device.index is not None else torch.cuda.current_device()
-            return ctypes.c_void_p(_raw_stream(idx))
+            return _raw_stream(idx)
         stream = torch.cuda.current_stream(device)
-    return ctypes.c_void_p(stream.cuda_stream)
+    return stream.cuda_stream
 
 
 def _dtype_code(t: torch.Tensor) -> int:
@@ -149,8 +151,17 @@ def abi_version() -> int:
     return lib().kb_abi_version()
 
 
+_ws_bytes_cache: dict = {}
+
+
 def kbest_workspace_bytes(dtype: int, N: int, H: int, V: int, k: int, S: int) -> int:
-    return int(lib().kb_kbest_workspace_bytes(dtype, N, H, V, k, S))
+    # a pure function of the shape (for one loaded library): asked once per shape
+    L = lib()
+    key = (id(L), dtype, N, H, V, k, S)
+    n = _ws_bytes_cache.get(key)
+    if n is None:
+        n = _ws_bytes_cache[key] = int(L.kb_kbest_workspace_bytes(dtype, N, H, V, k, S))
+    return n
 
 
 def workspace(nbytes: int, device=None) -> torch.Tensor:
@@ -485,13 +496,15 @@ def standin_alive(sid: torch.Tensor, lengths: torch.Tensor, S: int, k: int, t: i
 
 def standin_step(sid: torch.Tensor, lengths: torch.Tensor, score: torch.Tensor, S: int, k: int, t: int, *,
                  out: tuple, S_dev: Optional[torch.Tensor] = None, alive: Optional[torch.Tensor] = None,
-                 counts_host: Optional[torch.Tensor] = None, stream=None):
+                 counts_host: Optional[torch.Tensor] = None, next_state: Optional[tuple] = None, stream=None):
     """The loop step's bookkeeping in one launch (include/kbest_standin.h): the
     EOS mask, its compaction and the gathers of the surviving scores and sentence
     ids.  ``out`` = (keep_idx[S*k], counts[2], new_sent_offsets[S+1],
     prev_next[S*k] float32, sid_next[S]); returns it.  ``counts_host``, a pinned
-    int32 host tensor of 2, receives the counts too (readable once the step's
-    work has completed)."""
+    int32 host tensor of 3, receives the counts too, then the tag t + 1 (a host
+    that polls [2] may read [0] and [1] once the tag is there).  ``next_state`` = (table, T, next_h): the surviving
+    entries' states of step t + 1 gathered into next_h (rows x H, like table)
+    in the same launch."""
     keep, counts, noff, prev_next, sid_next = out
     _need(sid, "sid", dtype=torch.int32, numel=S)
     _need(lengths, "lengths", dtype=torch.int32)
@@ -508,11 +521,19 @@ def standin_step(sid: torch.Tensor, lengths: torch.Tensor, score: torch.Tensor, 
     if counts_host is not None:
         if not isinstance(counts_host, torch.Tensor) or counts_host.is_cuda or not counts_host.is_pinned():
             raise TypeError("counts_host must be a pinned host tensor")
-        if counts_host.dtype != torch.int32 or counts_host.numel() < 2 or not counts_host.is_contiguous():
-            raise ValueError("counts_host must be 2 contiguous int32")
+        if counts_host.dtype != torch.int32 or counts_host.numel() < 3 or not counts_host.is_contiguous():
+            raise ValueError("counts_host must be 3 contiguous int32")
+    table = next_h = None
+    T, row_bytes = 0, 0
+    if next_state is not None:
+        table, T, next_h = next_state
+        _need(table, "table", dim=2)
+        _need(next_h, "next_h", dtype=table.dtype, numel=S * k * table.shape[1])
+        row_bytes = table.shape[1] * table.element_size()
     _check(lib().kb_standin_step(S, _ptr(S_dev), k, t, _ptr(sid), _ptr(lengths), _ptr(score), _ptr(keep),
                                  _ptr(counts), _ptr(noff), _ptr(prev_next), _ptr(sid_next), _ptr(alive),
-                                 _ptr_host(counts_host), _stream(stream)))
+                                 _ptr_host(counts_host), _ptr(table), T, _ptr(next_h), row_bytes,
+                                 _stream(stream)))
     return out
 
 

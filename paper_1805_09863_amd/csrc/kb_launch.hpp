@@ -76,7 +76,7 @@ hipError_t launch_standin_alive(int S, const int32_t* S_dev, int k, int t, const
 hipError_t launch_standin_step(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
                                const float* score, int32_t* keep, int32_t* counts, int32_t* new_off,
                                float* prev_next, int32_t* sid_next, uint8_t* alive, int32_t* counts_host,
-                               hipStream_t st);
+                               const void* table, int T, void* next_h, size_t row_bytes, hipStream_t st);
 hipError_t launch_standin_next_h(int n_max, const int32_t* n_dev, int k, int T, int t, const int32_t* keep,
                                  const int32_t* sid, const void* table, void* out, size_t row_bytes,
                                  hipStream_t st);

@@ -111,18 +111,25 @@ bool dma_shape(int dtype, int H, int V) { return dtype == KB_BF16 && H % 128 == 
 
 // The few-row kernel holds every row's state in LDS next to its partial sums.
 constexpr size_t kFewLdsMax = 160 * 1024;
-// It streams W at about 4 TB/s and adds its arithmetic after the loads (about
-// 0.03-0.08 us per row and million weights), while the matrix-core kernels
-// carry about 20 us of fixed cost per step: it is the faster of the two up to
-// about 64 M row-weight products (measured on float32 and bf16 steps of 1-8
-// rows, H 256-2048, V 8k-90k).
-constexpr long long kFewMaxWork = 64ll << 20;
+// It streams W at 3.5-4 TB/s and adds its arithmetic after the loads, while
+// the matrix-core kernels carry about 20 us of fixed cost per step.  Measured
+// per step, both ways, at 1-8 rows: float32 (H 512-1024, V 30k, up to 234 M
+// row-weight products) it is 25-40% faster everywhere; bf16 it is faster at
+// V=50k, H=1024 up to 4 rows (195 M products; 32-36 against 32-37 us) and
+// slower from 6 rows, at V=90k (from one row: 47 against 41 us) and at
+// H=2048 (W of 88-102 M weights, where its bf16 dot products are the bound).
+constexpr long long kFewMaxWorkF32 = 1ll << 30;
+constexpr long long kFewMaxWorkBf16 = 200ll << 20;
+constexpr long long kFewMaxWeightsBf16 = 64ll << 20;
 
 Plan make_plan(int dtype, int N, int H, int V, int k, bool dma, bool vec) {
   Plan p{};
   const int few_cw = kb::few_chunk_words(dtype == KB_BF16);
   const int few_nt = (V + few_cw - 1) / few_cw, few_p = std::min(few_nt, kTargetCUs);
-  if (vec && N <= kb::FEW_ROWS && V >= few_cw && (long long)N * H * V <= kFewMaxWork &&
+  const long long few_work = (long long)N * H * V, few_weights = (long long)H * V;
+  const bool few_fits = dtype == KB_BF16 ? (few_work <= kFewMaxWorkBf16 && few_weights <= kFewMaxWeightsBf16)
+                                         : few_work <= kFewMaxWorkF32;
+  if (vec && N <= kb::FEW_ROWS && V >= few_cw && few_fits &&
       kb::few_lds_needed(dtype == KB_BF16, N, H, (few_nt + few_p - 1) / few_p) <= kFewLdsMax) {
     // a few rows: one pass over W on the vector ALUs; chunks of few_cw words,
     // as many splits as CUs (at most), each a run of whole chunks
@@ -753,15 +760,25 @@ kb_status kb_standin_alive(int S, const int32_t* S_dev, int k, int t, const int3
 
 kb_status kb_standin_step(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
                           const float* score, int32_t* keep_idx, int32_t* counts, int32_t* new_sent_offsets,
-                          float* prev_next, int32_t* sid_next, uint8_t* alive, int32_t* counts_host, void* stream) {
+                          float* prev_next, int32_t* sid_next, uint8_t* alive, int32_t* counts_host,
+                          const void* table, int T, void* next_h, size_t row_bytes, void* stream) {
   if (S < 0 || k < 1) return fail(KB_ERR_INVALID_ARG, "S = %d, k = %d", S, k);
   if ((long long)S * k > INT_MAX) return fail(KB_ERR_UNSUPPORTED, "S*k does not fit in int32");
   if (k >= (1 << 10)) return fail(KB_ERR_UNSUPPORTED, "k = %d: at most 1023 entries per sentence", k);
   if (!counts || !new_sent_offsets) return fail(KB_ERR_INVALID_ARG, "null counts or new_sent_offsets");
   if (S > 0 && (!sid || !lengths || !score || !keep_idx || !prev_next || !sid_next))
     return fail(KB_ERR_INVALID_ARG, "null sid, lengths, score, keep_idx, prev_next or sid_next");
+  if (next_h) {
+    if (!table) return fail(KB_ERR_INVALID_ARG, "null table with next_h");
+    if (t < 0 || T < 1 || t + 1 >= T) return fail(KB_ERR_INVALID_ARG, "t = %d, T = %d: next states need t + 1 < T", t, T);
+    if (row_bytes == 0 || row_bytes % 4 != 0)
+      return fail(KB_ERR_INVALID_ARG, "row_bytes must be a positive multiple of 4");
+    if (row_bytes / 4 > INT_MAX) return fail(KB_ERR_UNSUPPORTED, "row too long");
+    if (!aligned(table, 4) || !aligned(next_h, 4))
+      return fail(KB_ERR_INVALID_ARG, "table and next_h must be 4-byte aligned");
+  }
   hipError_t e = kb::launch_standin_step(S, S_dev, k, t, sid, lengths, score, keep_idx, counts, new_sent_offsets,
-                                         prev_next, sid_next, alive, counts_host,
+                                         prev_next, sid_next, alive, counts_host, table, T, next_h, row_bytes,
                                          reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(KB_ERR_HIP, "stand-in step kernel launch: %s", hipGetErrorString(e));
   return ok();

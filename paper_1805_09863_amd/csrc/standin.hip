@@ -8,10 +8,12 @@
 //     reaches its drawn length this step (every continuation ends together);
 //   * standin_next_h: the next step's state of each surviving entry, read
 //     from the table at (original sentence id, step, beam slot);
-//   * standin_step: the mask, the compaction over it (K3's scan) and the
-//     gathers of the surviving entries' scores and sentences' ids, in one
-//     launch of one workgroup: a loop step is then the output layer, this,
-//     and the next states.
+//   * standin_step: the mask, the compaction over it (K3's scan), the
+//     gathers of the surviving entries' scores and sentences' ids and,
+//     optionally, of their next states, in one launch: a loop step is then
+//     the output layer and this.
+#include <algorithm>
+
 #include "k3_scan.hpp"
 
 namespace kb {
@@ -44,49 +46,75 @@ __global__ __launch_bounds__(256) void standin_next_h(int n_max, const int32_t* 
   }
 }
 
+// One step's bookkeeping.  Workgroup 0 writes the compaction's outputs
+// (surviving entries and their scores, new offsets, surviving sentences'
+// ids, the counts, optionally the mask).  With next_h, every workgroup also
+// gathers its share of the surviving entries' next states from the table;
+// each works the compaction out again for itself (a scan over the S*k entries
+// into its LDS), so no workgroup waits for another and the step's
+// bookkeeping is one launch.
+template <class V>
 __global__ __launch_bounds__(K3_T) void standin_step(int S, const int32_t* __restrict__ S_dev, int k, int t,
                                                      const int32_t* __restrict__ sid,
                                                      const int32_t* __restrict__ lengths,
                                                      const float* __restrict__ score, int32_t* __restrict__ keep,
                                                      int32_t* __restrict__ counts, int32_t* __restrict__ new_off,
                                                      float* __restrict__ prev_next, int32_t* __restrict__ sid_next,
-                                                     uint8_t* __restrict__ alive, int32_t* __restrict__ counts_host) {
+                                                     uint8_t* __restrict__ alive, int32_t* __restrict__ counts_host,
+                                                     const V* __restrict__ table, int T, V* __restrict__ next_h,
+                                                     int row_words) {
   __shared__ int wsum[K3_W];
+  extern __shared__ int keep_l[];  // [S*k] the surviving entries (with next_h only)
   const int tid = threadIdx.x;
+  const bool lead = blockIdx.x == 0;
   const int live = S_dev ? min(S, *S_dev) : S;  // sentences past it do not exist this step
   auto is_alive = [&](int e) {
     const int s = e / k;
     return s < live && t < lengths[sid[s]] - 1;
   };
   const int kept = compact_entries_pass(S * k, is_alive, [&](int o, int e) {
-    keep[o] = e;
-    prev_next[o] = score[e];
+    if (lead) {
+      keep[o] = e;
+      prev_next[o] = score[e];
+    }
+    if (next_h) keep_l[o] = e;
   }, wsum);
-  int sbase, ebase;
-  compact_sentences_pass(S, k, is_alive, [&](int pos, int s, int first) {
-    new_off[pos] = first;
-    sid_next[pos] = sid[s];
-  }, wsum, sbase, ebase);
-  for (int s = sbase + tid; s <= S; s += K3_T) new_off[s] = ebase;  // empty sentences past the survivors
-  if (alive)
-    for (int e = tid; e < S * k; e += K3_T) alive[e] = is_alive(e) ? 1 : 0;
-  if (tid == 0) {
-    counts[0] = kept;
-    counts[1] = sbase;
-    if (counts_host) {  // pinned host memory: visible to the host once the kernel has completed
-      counts_host[0] = kept;
-      counts_host[1] = sbase;
+  if (lead) {
+    int sbase, ebase;
+    compact_sentences_pass(S, k, is_alive, [&](int pos, int s, int first) {
+      new_off[pos] = first;
+      sid_next[pos] = sid[s];
+    }, wsum, sbase, ebase);
+    for (int s = sbase + tid; s <= S; s += K3_T) new_off[s] = ebase;  // empty sentences past the survivors
+    if (alive)
+      for (int e = tid; e < S * k; e += K3_T) alive[e] = is_alive(e) ? 1 : 0;
+    if (tid == 0) {
+      counts[0] = kept;
+      counts[1] = sbase;
+      if (counts_host) {
+        // pinned host memory: the counts, then the step's tag t + 1, each
+        // pushed out by a system-scope fence, so a host that sees the tag sees
+        // the counts (before the kernel has completed)
+        counts_host[0] = kept;
+        counts_host[1] = sbase;
+        __threadfence_system();
+        counts_host[2] = t + 1;
+        __threadfence_system();
+      }
     }
   }
-}
-
-hipError_t launch_standin_step(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
-                               const float* score, int32_t* keep, int32_t* counts, int32_t* new_off,
-                               float* prev_next, int32_t* sid_next, uint8_t* alive, int32_t* counts_host,
-                               hipStream_t st) {
-  standin_step<<<dim3(1), dim3(K3_T), 0, st>>>(S, S_dev, k, t, sid, lengths, score, keep, counts, new_off, prev_next,
-                                              sid_next, alive, counts_host);
-  return hipGetLastError();
+  if (next_h) {
+    __syncthreads();  // keep_l complete
+    // this workgroup's surviving rows: an even share of the S*k the launch was sized for
+    const int per = (S * k + (int)gridDim.x - 1) / (int)gridDim.x;
+    const int r0 = min((int)blockIdx.x * per, kept), r1 = min(r0 + per, kept);
+    for (int i = r0 * row_words + tid; i < r1 * row_words; i += K3_T) {
+      const int r = i / row_words, w = i - r * row_words;
+      const int e = keep_l[r];
+      const long long src = ((long long)sid[e / k] * T + t + 1) * k + e % k;
+      next_h[i] = table[src * row_words + w];
+    }
+  }
 }
 
 hipError_t launch_standin_alive(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
@@ -112,6 +140,61 @@ hipError_t launch_standin_next_h(int n_max, const int32_t* n_dev, int k, int T, 
     standin_next_h<uint32_t><<<dim3(blocks), dim3(256), 0, st>>>(n_max, n_dev, k, T, t, keep, sid,
                                                                  (const uint32_t*)table, (uint32_t*)out,
                                                                  (int)words);
+  return hipGetLastError();
+}
+
+// The fused gather keeps the surviving entries in LDS: at most this many.
+constexpr int kStandinFusedMax = 16384;
+
+hipError_t launch_standin_step(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
+                               const float* score, int32_t* keep, int32_t* counts, int32_t* new_off,
+                               float* prev_next, int32_t* sid_next, uint8_t* alive, int32_t* counts_host,
+                               const void* table, int T, void* next_h, size_t row_bytes, hipStream_t st) {
+  const long long M = (long long)S * k;
+  const bool v16 = (row_bytes % 16 == 0) && ((uintptr_t)table % 16 == 0) && ((uintptr_t)next_h % 16 == 0);
+  const long long words = next_h ? (long long)(v16 ? row_bytes / 16 : row_bytes / 4) : 0;
+  if (next_h && (M > kStandinFusedMax || M * words > INT_MAX)) {
+    // too many entries for one workgroup's LDS: the bookkeeping, then the gather
+    standin_step<uint32_t><<<dim3(1), dim3(K3_T), 0, st>>>(S, S_dev, k, t, sid, lengths, score, keep, counts, new_off,
+                                                        prev_next, sid_next, alive, counts_host, nullptr, 0,
+                                                        nullptr, 0);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_standin_next_h((int)M, counts, k, T, t + 1, keep, sid, table, next_h, row_bytes, st);
+  }
+  if (!next_h) {
+    standin_step<uint32_t><<<dim3(1), dim3(K3_T), 0, st>>>(S, S_dev, k, t, sid, lengths, score, keep, counts, new_off,
+                                                        prev_next, sid_next, alive, counts_host, nullptr, 0,
+                                                        nullptr, 0);
+    return hipGetLastError();
+  }
+  // one workgroup per 32 KB of states (at most 256): each works out the scan
+  // again, which costs little next to its share of the copy
+  const long long bytes = M * (long long)row_bytes;
+  const int G = (int)std::min<long long>(std::max<long long>((bytes + (32 << 10) - 1) >> 15, 1), 256);
+  const size_t lds = (size_t)std::max<long long>(M, 1) * sizeof(int32_t);
+  if (lds > 48 * 1024) {
+    static bool attr_set[2] = {false, false};  // the LDS ceiling, raised once per process and variant
+    if (!attr_set[v16]) {
+      const hipError_t e = v16 ? hipFuncSetAttribute(reinterpret_cast<const void*>(&standin_step<uint4>),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                     kStandinFusedMax * (int)sizeof(int32_t))
+                               : hipFuncSetAttribute(reinterpret_cast<const void*>(&standin_step<uint32_t>),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                     kStandinFusedMax * (int)sizeof(int32_t));
+      if (e != hipSuccess) return e;
+      attr_set[v16] = true;
+    }
+  }
+  if (v16)
+    standin_step<uint4><<<dim3(G), dim3(K3_T), lds, st>>>(S, S_dev, k, t, sid, lengths, score, keep, counts, new_off,
+                                                         prev_next, sid_next, alive, counts_host,
+                                                         (const uint4*)table, T, (uint4*)next_h, (int)words);
+  else
+    standin_step<uint32_t><<<dim3(G), dim3(K3_T), lds, st>>>(S, S_dev, k, t, sid, lengths, score, keep, counts,
+                                                            new_off, prev_next, sid_next, alive, counts_host,
+                                                            (const uint32_t*)table, T, (uint32_t*)next_h,
+                                                            (int)words);
   return hipGetLastError();
 }
 

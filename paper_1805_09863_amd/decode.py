@@ -11,12 +11,39 @@ runs in its own small kernels (include/kbest_standin.h).
 """
 from __future__ import annotations
 
+import time
 from dataclasses import dataclass, field
 from typing import Callable, Optional
 
 import torch
 
 from . import binding as kbb
+
+
+def _poll_tag(cn, tag: int):
+    """Wait until the kernel has written ``tag`` to cn[2] (pinned host memory,
+    after the counts it guards): no event is recorded or waited on per step
+    (an event cost the device about 6 us a step).  A tag that does not come
+    within a second leads to a device synchronisation, which raises if the
+    device has failed, and then to an error."""
+    n = 0
+    while cn[2] != tag:
+        n += 1
+        if n & 0xFFFF == 0:
+            if n == 0x10000:
+                t0 = time.perf_counter()
+            elif time.perf_counter() - t0 > 1.0:
+                torch.cuda.synchronize()
+                if cn[2] != tag:
+                    raise RuntimeError(f"step tag {tag} never arrived (found {int(cn[2])})")
+
+
+def _wait(ev: torch.cuda.Event):
+    """Wait for ev by polling.  The wait covers most of a step, and a blocking
+    wait of that length woke the host tens of microseconds after the event, by
+    which time the device had drained the one step queued behind it."""
+    while not ev.query():
+        pass
 
 
 @dataclass
@@ -43,9 +70,9 @@ def decode_loop(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, lengths
     ``compact=False``: the batch keeps all S0 sentences until the longest is
     done (Algorithm 1); finished sentences' rows are decoded and ignored.
 
-    A compacted step enqueues the output layer, the stand-in's step (EOS
-    mask, compaction, gathers of the surviving scores and sentence ids: one
-    launch) and the stand-in's next states.  The batch only shrinks, so step
+    A compacted step enqueues the output layer and the stand-in's step (EOS
+    mask, compaction, gathers of the surviving scores, sentence ids and next
+    states: one launch).  The batch only shrinks, so step
     t + 1 is launched sized by the exact counts of step t (rows, sentences), read from the
     device while step t is still queued: the host never waits for the step it
     has just launched, and the device never waits for the host.  Every kernel
@@ -99,32 +126,57 @@ def decode_loop(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, lengths
         prev_nx = torch.zeros(M0, dtype=torch.float32, device=dev)
         sid_nx = torch.empty(S0, **i32)
         # counts (kept rows, kept sentences) of each step, double-buffered on
-        # both sides: step t writes slot t % 2, read back one step later
+        # both sides: step t writes slot t % 2, read back one step later; the
+        # host copy carries the step's tag t + 1 after the counts (0: none yet)
         cnt = [torch.empty(2, **i32) for _ in range(2)]
-        cnt_host = [torch.empty(2, dtype=torch.int32, pin_memory=True) for _ in range(2)]
-        ready = [torch.cuda.Event(), torch.cuda.Event()]
-        S_ex = None                                      # the device's count of the current batch's sentences
+        cnt_host = [torch.zeros(3, dtype=torch.int32, pin_memory=True) for _ in range(2)]
+        # A step's host work bounds small batches (its device work is a few
+        # tens of us), so the buffers are checked once here, at the largest
+        # batch, as the binding checks them, and the steps call the library
+        # with their cached addresses (no per-step tensor views or checks).
+        f32, i32t = torch.float32, torch.int32
+        for name, x, d, n in (("h", h_cur, h_table.dtype, M0 * H), ("h_next", h_nx, h_table.dtype, M0 * H),
+                              ("W", W, h_table.dtype, H * V), ("b", b, f32, V), ("prev", prev, f32, M0),
+                              ("prev_next", prev_nx, f32, M0), ("sent_offsets", off, i32t, S0 + 1),
+                              ("new_sent_offsets", noff, i32t, S0 + 1), ("token", tok, i32t, M0),
+                              ("parent", par, i32t, M0), ("score", sc, f32, M0), ("keep", keep, i32t, M0),
+                              ("sid", sid, i32t, S0), ("sid_next", sid_nx, i32t, S0), ("lengths", lengths, i32t, S0),
+                              ("table", h_table, h_table.dtype, S0 * T * k * H), ("counts", cnt[0], i32t, 2),
+                              ("counts", cnt[1], i32t, 2), ("ws", ws, None, None)):
+            kbb._need(x, name, dtype=d, numel=n)
+        if h_table.dim() != 2 or h_table.shape[1] != H:
+            raise ValueError("h_table must be rows x H")
+        L = kbb.lib()
+        st_h = kbb._stream(stream, dev)
+        Wp, bp, tokp, parp, scp, keepp = (x.data_ptr() for x in (W, b, tok, par, sc, keep))
+        lenp, tabp, wsp, ws_bytes = lengths.data_ptr(), h_table.data_ptr(), ws.data_ptr(), ws.numel()
+        row_bytes = H * h_table.element_size()
+        cnt_p = [c.data_ptr() for c in cnt]
+        cnt_hp = [c.data_ptr() for c in cnt_host]
+        cnt_np = [c.numpy() for c in cnt_host]          # views of the pinned counts
+        hp, hnp = h_cur.data_ptr(), h_nx.data_ptr()
+        pp, pnp = prev.data_ptr(), prev_nx.data_ptr()
+        sidp, sidnp = sid.data_ptr(), sid_nx.data_ptr()
+        offp, noffp = off.data_ptr(), noff.data_ptr()
+        S_exp = None                                    # the device's count of the current batch's sentences
         while t < T:
-            c = cnt[t % 2]
-            kbb.kbest_step(h_cur[:N], W, b, prev[:N], off[:S + 1], k, S=S,
-                           out=(tok[:S * k].view(S, k), par[:S * k].view(S, k), sc[:S * k].view(S, k)),
-                           ws=ws, stream=stream)
-            # EOS mask, compaction, surviving scores and sentence ids: one launch
-            # (the counts also land in pinned host memory, read once the step is done)
-            kbb.standin_step(sid[:S], lengths, sc[:S * k], S, k, t,
-                             out=(keep[:S * k], c, noff[:S + 1], prev_nx[:S * k], sid_nx[:S]), S_dev=S_ex,
-                             counts_host=cnt_host[t % 2], stream=stream)
-            ready[t % 2].record(stream)
-            if t + 1 < T:
-                kbb.standin_next_h(h_table, keep, sid, k, T, t + 1, S * k, n_dev=c[0:1], out=h_nx,
-                                   stream=stream)
+            kbb._check(L.kb_kbest_step(dt, N, H, V, k, S, hp, Wp, bp, pp, offp, tokp, parp, scp, None, wsp,
+                                       ws_bytes, st_h))
+            # EOS mask, compaction, surviving scores, sentence ids and next states:
+            # one launch (the counts also land in pinned host memory, read once
+            # the step is done)
+            nxt = t + 1 < T
+            kbb._check(L.kb_standin_step(S, S_exp, k, t, sidp, lenp, scp, keepp, cnt_p[t % 2], noffp, pnp, sidnp,
+                                         None, cnt_hp[t % 2], tabp if nxt else None, T, hnp if nxt else None,
+                                         row_bytes, st_h))
             stats.launch_rows.append(N)
             # the exact counts of this step's batch: the previous step's output
             if t == 0:
                 N_ex, S_now = M0, S0
             else:
-                ready[(t - 1) % 2].synchronize()
-                N_ex, S_now = (int(x) for x in cnt_host[(t - 1) % 2].tolist())
+                cn = cnt_np[(t - 1) % 2]
+                _poll_tag(cn, t)
+                N_ex, S_now = int(cn[0]), int(cn[1])
             if N_ex == 0:
                 break                                    # every sentence had ended: this launch was empty
             stats.rows.append(N_ex)
@@ -134,11 +186,11 @@ def decode_loop(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, lengths
                                 score=sc[:S_now * k].view(S_now, k), S=S_now, N=N_ex, S_launch=S, N_launch=N,
                                 token_launch=tok[:S * k].view(S, k), score_launch=sc[:S * k].view(S, k)))
             N, S = N_ex, S_now                           # bounds of the next step's batch
-            S_ex = c[1:2]
-            prev, prev_nx = prev_nx, prev
-            sid, sid_nx = sid_nx, sid
-            off, noff = noff, off
-            h_cur, h_nx = h_nx, h_cur
+            S_exp = cnt_p[t % 2] + 4                     # counts[1] of this step
+            prev, prev_nx, pp, pnp = prev_nx, prev, pnp, pp
+            sid, sid_nx, sidp, sidnp = sid_nx, sid, sidnp, sidp
+            off, noff, offp, noffp = noff, off, noffp, offp
+            h_cur, h_nx, hp, hnp = h_nx, h_cur, hnp, hp
             t += 1
     else:
         while t < Lmax:
@@ -247,7 +299,7 @@ def beam_search(h_table: torch.Tensor, W: torch.Tensor, b: torch.Tensor, k: int,
                         stream=stream)
         if t + 1 < T:
             kbb.standin_next_h(h_table, keep[cur], sid, k, T, t + 1, S * k, n_dev=cnt[0:1], out=h_cur, stream=stream)
-        ready.synchronize()                            # the step's one host sync
+        _wait(ready)                                   # the step's one host sync
         N, S = (int(x) for x in cnt_host.tolist())
         prev, prev_nx = prev_nx, prev
         sid, sid_nx = sid_nx, sid

@@ -53,7 +53,8 @@ def test_standin_argument_checks():
 
 def test_standin_step_argument_checks():
     L = binding.lib()
-    st = lambda *a: L.kb_standin_step(*a[:13], None, a[13])   # noqa: E731  (no host copy of the counts)
+    # no host copy of the counts, no state gather
+    st = lambda *a: L.kb_standin_step(*a[:13], None, None, 0, None, 0, a[13])   # noqa: E731
     F = FAKE
     assert st(-1, None, 5, 0, F, F, F, F, F, F, F, F, None, None) == KB_ERR_INVALID_ARG
     assert st(3, None, 0, 0, F, F, F, F, F, F, F, F, None, None) == KB_ERR_INVALID_ARG
@@ -63,6 +64,15 @@ def test_standin_step_argument_checks():
         args = [3, None, 5, 0] + [F] * 8 + [None, None]
         args[i] = None
         assert st(*args) == KB_ERR_INVALID_ARG, f"argument {i} may not be null"
+    # with the next states: (table, T, next_h, row_bytes)
+    nx = lambda t, table, T, nh, rb: L.kb_standin_step(3, None, 5, t, F, F, F, F, F, F, F, F, None, None,  # noqa: E731
+                                                       table, T, nh, rb, None)
+    assert nx(0, None, 60, F, 2048) == KB_ERR_INVALID_ARG                      # no table
+    assert nx(59, F, 60, F, 2048) == KB_ERR_INVALID_ARG                        # t + 1 == T: no next step
+    assert nx(-1, F, 60, F, 2048) == KB_ERR_INVALID_ARG
+    assert nx(0, F, 60, F, 6) == KB_ERR_INVALID_ARG                            # row bytes % 4
+    assert nx(0, F, 60, F, 0) == KB_ERR_INVALID_ARG
+    assert nx(0, F, 60, ctypes.c_void_p(0x1002), 2048) == KB_ERR_INVALID_ARG   # misaligned next_h
 
 
 def test_abi_version_and_status_strings():
@@ -342,7 +352,8 @@ def test_every_pointer_the_binding_passes_was_checked(monkeypatch):
                            out=z(S * k, H, d=bf), stream=st)
     binding.standin_step(z(S, d=i32), z(4, d=i32), z(S * k), S, k, 0,
                          out=(z(S * k, d=i32), z(2, d=i32), z(S + 1, d=i32), z(S * k), z(S, d=i32)),
-                         S_dev=z(1, d=i32), alive=z(S * k, d=u8), stream=st)
+                         S_dev=z(1, d=i32), alive=z(S * k, d=u8), next_state=(z(40, H, d=bf), 4, z(S * k, H, d=bf)),
+                         stream=st)
     fin = (z(4, d=i32), z(4 * k), z(4 * k, d=i32), z(4 * k, d=i32))
     binding.beam_finish(S, k, 0, 4, 1, out3[0], out3[1], out3[2], z(S, d=i32), z(S, d=i32), z(S, d=i32), 0, 0,
                         z(4 * S * k, d=i32), z(4 * S * k, d=i32), fin, z(S * k, d=u8), stream=st)

@@ -109,15 +109,20 @@ def test_standin_alive_device_count(kb, S_live):
     assert np.array_equal(alive.cpu().numpy(), want)
 
 
-@pytest.mark.parametrize("S,k,S_live", [(0, 5, None), (20, 3, None), (20, 3, 0), (20, 3, 9), (1, 5, None), (512, 5, 300),
-                                         (1500, 4, 1400), (2048, 12, None)])
-def test_standin_step_matches_its_definition(kb, S, k, S_live):
+@pytest.mark.parametrize("S,k,S_live,H", [(0, 5, None, 8), (20, 3, None, 5), (20, 3, 0, 8), (20, 3, 9, 8),
+                                           (1, 5, None, 5), (512, 5, 300, 8), (1500, 4, 1400, 5),
+                                           (2048, 12, None, 8)])
+@pytest.mark.parametrize("gather", [False, True])
+def test_standin_step_matches_its_definition(kb, S, k, S_live, H, gather):
     # the fused step = the stand-in's EOS mask, the stable compaction of that
-    # mask (np.flatnonzero), the sentence offsets and the two gathers; sentences
-    # past the device count are dropped without reading their (stale) ids
+    # mask (np.flatnonzero), the sentence offsets and the gathers (scores,
+    # sentence ids and, with gather, the next states: 16-byte rows at H = 8,
+    # 4-byte words at H = 5; one launch up to 16384 entries, two past it at
+    # 2048 x 12); sentences past the device count are dropped without reading
+    # their (stale) ids
     from paper_1805_09863_amd import binding as kbb
     g = np.random.default_rng(S * 7 + k)
-    t = 6
+    t, T = 6, 8
     n_orig = S + 40
     lengths = g.integers(1, 14, n_orig).astype(np.int32)
     lengths[n_orig - 1] = 13                      # the stale id below: would read as alive
@@ -139,13 +144,15 @@ def test_standin_step_matches_its_definition(kb, S, k, S_live):
     sid_next = torch.full((S,), -9, dtype=torch.int32, device="cuda")
     alive = torch.full((S * k,), 7, dtype=torch.uint8, device="cuda")
     s_dev = None if S_live is None else torch.tensor([S_live], dtype=torch.int32, device="cuda")
-    counts_host = torch.full((2,), -9, dtype=torch.int32, pin_memory=True)
+    counts_host = torch.full((3,), -9, dtype=torch.int32, pin_memory=True)
+    table = torch.from_numpy(g.standard_normal((n_orig * T * k, H)).astype(np.float32)).cuda()
+    nh = torch.full((S * k, H), float("nan"), dtype=torch.float32, device="cuda")
     kbb.standin_step(sid_dev, torch.from_numpy(lengths).cuda(), torch.from_numpy(score).cuda(), S, k, t,
                      out=(keep, counts, noff, prev_next, sid_next), S_dev=s_dev, alive=alive,
-                     counts_host=counts_host)
+                     counts_host=counts_host, next_state=(table, T, nh) if gather else None)
     torch.cuda.synchronize()
     n, ns = (int(x) for x in counts.cpu())
-    assert counts_host.tolist() == [n, ns]        # the copy the kernel writes to pinned host memory
+    assert counts_host.tolist() == [n, ns, t + 1]  # the copy the kernel writes to pinned host memory, and the tag
     assert (n, ns) == (keep_want.size, ks.size)
     assert np.array_equal(keep.cpu().numpy()[:n], keep_want)
     assert np.array_equal(alive.cpu().numpy(), mask.astype(np.uint8))
@@ -154,6 +161,11 @@ def test_standin_step_matches_its_definition(kb, S, k, S_live):
     assert (noff_h[ns:] == n).all()               # empty sentences past the survivors
     assert np.array_equal(prev_next.cpu().numpy()[:n].view(np.uint32), score[keep_want].view(np.uint32))
     assert np.array_equal(sid_next.cpu().numpy()[:ns], sid[ks])
+    nh_h = nh.cpu().numpy()
+    if gather:
+        src = (sid[keep_want // k].astype(np.int64) * T + t + 1) * k + keep_want % k
+        assert np.array_equal(nh_h[:n].view(np.uint32), table.cpu().numpy()[src].view(np.uint32))
+    assert np.isnan(nh_h[n:]).all()               # rows past the survivors are not written
 
 
 # ---------------------------------------------------------------- the M-entry form (kb_compact_batch)

@@ -27,7 +27,7 @@ def kb():
 
 
 FEW = [
-    # (rows per sentence, H, V, k, dtype); N * H * V <= 64 M (the planner's limit)
+    # (rows per sentence, H, V, k, dtype): shapes the planner gives the few-row kernel
     ([1], 256, 8000, 1, "f32"),                 # one row, k = 1
     ([5], 256, 8000, 5, "bf16"),
     ([1], 1024, 60000, 16, "bf16"),             # 2 chunks per split, k = 16

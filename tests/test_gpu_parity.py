@@ -39,13 +39,14 @@ SMALL = [
     ([1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15, 16, 17], 64, 5000, 7, "f32"),
     ([40, 3], 64, 60000, 16, "bf16"),          # many splits per row, a sentence of 40 rows
     ([20, 17, 1], 64, 30000, 13, "f32"),       # sentences longer than one merge chunk
-    # few rows: the word tile (512, 256 or 128) follows the vocabulary size
-    ([5], 256, 50000, 5, "bf16"),              # 256-word tiles, DMA pipeline
-    ([3, 2], 128, 20000, 4, "bf16"),           # 128-word tiles, DMA pipeline
+    # 9-64 rows (8 or fewer go to the few-row kernel, tests/test_gpu_few.py):
+    # the word tile (512, 256 or 128) follows the vocabulary size
+    ([5, 5], 256, 50000, 5, "bf16"),           # 256-word tiles, DMA pipeline
+    ([3, 2, 4], 128, 20000, 4, "bf16"),        # 128-word tiles, DMA pipeline
     ([2] * 10, 128, 40000, 12, "bf16"),        # 256-word tiles, k = 12
-    ([4, 4], 64, 40000, 3, "f32"),             # 256-word tiles, register-staged f32
+    ([4, 4, 1], 64, 40000, 3, "f32"),          # 256-word tiles, register-staged f32
     ([16, 16], 128, 70000, 16, "bf16"),        # 512-word tiles, k = 16, 32 rows
-    ([2, 3, 1], 128, 20000, 2, "bf16"),        # k = 2: merge lanes staged in pairs
+    ([2, 3, 1, 3], 128, 20000, 2, "bf16"),     # k = 2: merge lanes staged in pairs
     ([10] * 5, 128, 20000, 6, "bf16"),         # 50 rows: two 32-row tiles, DMA pipeline
     ([16] * 4, 256, 30000, 16, "bf16"),        # 64 rows: two full 32-row tiles, k = 16
     ([13] * 7, 128, 8000, 5, "bf16"),          # 91 rows: one 128-row tile, DMA pipeline
