@@ -311,7 +311,7 @@ def configs_bench(torch, np, kb, reps: int = 50):
         out = tuple(torch.empty((S, k), dtype=t, device="cuda") for t in (torch.int32, torch.int32, torch.float32))
         ws = kb.workspace(kb.kbest_workspace_bytes(dt, N, H, V, k, S))
         step = lambda events=None: kb.kbest_step(h, W, b, prev, off, k, out=out, ws=ws, events=events)
-        for _ in range(10):
+        for _ in range(50):                # the clock settles over the first ~40 launches of a heavy step
             step()
         torch.cuda.synchronize()
         pairs = [(ev.create(), ev.create()) for _ in range(reps)]
