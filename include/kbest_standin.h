@@ -46,8 +46,8 @@ kb_status kb_standin_alive(int S, const int32_t* S_dev, int k, int t, const int3
  * entries' scores and the surviving sentences' original ids to the next
  * step, and, if next_h is given, the gather of kb_standin_next_h for step
  * t + 1 (the surviving entries' next states).
- *   S, S_dev, k, t, sid, lengths   as kb_standin_alive (sid is read only for
- *              sentences below min(S, *S_dev)).
+ *   S, S_dev, k, t, sid, lengths   as kb_standin_alive (ids at or past
+ *              min(S, *S_dev) are not used; see below).
  *   score      S*k float32, the step's scores (kb_kbest_step's out_score).
  *   keep_idx   S*k int32 out: the surviving entries in order (first counts[0]).
  *   counts     2 int32 out: [0] surviving entries, [1] surviving sentences.
@@ -69,11 +69,13 @@ kb_status kb_standin_alive(int S, const int32_t* S_dev, int k, int t, const int3
  *              t + 1 < T, row_bytes a positive multiple of 4, table and
  *              next_h 4-byte aligned.  Rows past counts[0] are not written.
  * Buffers are distinct, caller-owned device memory (counts_host aside).  S == 0 writes counts = 0
- * and new_sent_offsets[0] = 0.  1 <= k < 1024; S*k fits in int32.  Workgroup
- * 0 does the bookkeeping; with next_h every workgroup (one per 32 KB of
- * states) also works the compaction out in its own LDS and gathers its share
- * of the states, so the whole step is one launch up to 16384 entries (two
- * launches above).  KB_ERR_INVALID_ARG for null required pointers or bad sizes.
+ * and new_sent_offsets[0] = 0.  1 <= k < 1024; S*k fits in int32.  sid[s]
+ * may be read for every s < S, but an id is used (to index lengths) only
+ * below min(S, *S_dev).  Workgroup 0 does the bookkeeping; with next_h the
+ * other workgroups (one per 32 KB of states) each work the compaction out
+ * again in their own LDS and gather their share of the states, so the whole
+ * step is one launch while S*k + S + 1 int32 fit in 64 KB (two launches
+ * above).  KB_ERR_INVALID_ARG for null required pointers or bad sizes.
  */
 kb_status kb_standin_step(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
                           const float* score, int32_t* keep_idx, int32_t* counts, int32_t* new_sent_offsets,

@@ -62,8 +62,11 @@ __device__ __forceinline__ float wave_sum(float v) {
 // and flat index: a higher score, then a lower flat index, gives the larger key.
 __device__ __forceinline__ uint64_t cand_key(float score, int flat) { return key_of(score, flat); }
 
-template <int NQ>  // split lists per lane: P <= 64 * NQ
-__global__ __launch_bounds__(1024) void k2_merge(K2Args a) {
+// NQ: split lists per lane (P <= 64 * NQ); MAXT: the workgroup size it is
+// compiled for (1024: up to 16 waves, 128 VGPRs; 512: up to 8, 256 VGPRs,
+// which lets a lane keep a whole row's staging loads in flight)
+template <int NQ, int MAXT>
+__global__ __launch_bounds__(MAXT) void k2_merge(K2Args a) {
   __shared__ __align__(16) uint64_t key[K2_C];  // read two at a time when ranked
   __shared__ int c_t[K2_C];
   __shared__ int c_p[K2_C];
@@ -114,10 +117,12 @@ __global__ __launch_bounds__(1024) void k2_merge(K2Args a) {
       // lane = kp * g + j (kp: k rounded up to a power of two) stages entry j
       // of lists p0 + g, p0 + gpl + g, ... (gpl = 64 / kp lists per load;
       // slots k .. kp - 1 get empty entries): LB loads in flight per lane
-      // before the first LDS write (16 while the registers allow, 8 for the
-      // longest split counts).  Slots past kp are never read before a list
-      // has given up all k entries, so they stay unwritten.
-      constexpr int LB = NQ <= 2 ? 16 : 8;
+      // before the first LDS write (as many as the registers allow: 32 in the
+      // 512-thread form, whose row of up to 256 splits then takes one batch
+      // up to k = 8; 16, or 8 for the longest split counts, in the 1024-thread
+      // form).  Slots past kp are never read before a list has given up all
+      // k entries, so they stay unwritten.
+      constexpr int LB = MAXT <= 512 ? 32 : (NQ <= 2 ? 16 : 8);
       const int lgk = k <= 1 ? 0 : (k <= 2 ? 1 : (k <= 4 ? 2 : (k <= 8 ? 3 : 4)));
       const int j = lane & ((1 << lgk) - 1), g = lane >> lgk, gpl = 64 >> lgk;
       for (int p0 = 0; p0 < P; p0 += LB * gpl) {
@@ -274,6 +279,20 @@ hipError_t launch_k2_argmax(const int2* lists, int P, int N, int32_t* tok, float
   return hipGetLastError();
 }
 
+template <int NQ, int MAXT>
+static hipError_t launch_k2_w(const K2Args& a, int W, size_t lds, hipStream_t st) {
+  static bool attr_set = false;  // the kernel's LDS ceiling (at most 144 KB + one list), raised once per process
+  if (lds > 48 * 1024 && !attr_set) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k2_merge<NQ, MAXT>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             (int)(K2_LS * sizeof(int2) + 144 * 1024));
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  k2_merge<NQ, MAXT><<<dim3(a.S), dim3(64 * W), lds, st>>>(a);
+  return hipGetLastError();
+}
+
 template <int NQ>
 static hipError_t launch_k2_nq(const K2Args& a, hipStream_t st) {
   // one wave per row of a sentence of average length (longer sentences take
@@ -283,16 +302,7 @@ static hipError_t launch_k2_nq(const K2Args& a, hipStream_t st) {
   const int rows_per = (a.N + a.S - 1) / a.S;
   const int W = (int)std::min<size_t>(std::min(K2_MAXW, std::max(1, rows_per)), (144 * 1024) / per_wave);
   const size_t lds = (size_t)K2_LS * sizeof(int2) + (size_t)W * per_wave;
-  static bool attr_set = false;  // the kernel's LDS ceiling (at most 144 KB + one list), raised once per process
-  if (lds > 48 * 1024 && !attr_set) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k2_merge<NQ>),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize,
-                                             (int)(K2_LS * sizeof(int2) + 144 * 1024));
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  k2_merge<NQ><<<dim3(a.S), dim3(64 * W), lds, st>>>(a);
-  return hipGetLastError();
+  return W <= 8 ? launch_k2_w<NQ, 512>(a, W, lds, st) : launch_k2_w<NQ, 1024>(a, W, lds, st);
 }
 
 // A vocabulary shard's partial lists hold shard-local words; this moves them

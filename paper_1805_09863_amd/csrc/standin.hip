@@ -64,14 +64,21 @@ __global__ __launch_bounds__(K3_T) void standin_step(int S, const int32_t* __res
                                                      const V* __restrict__ table, int T, V* __restrict__ next_h,
                                                      int row_words) {
   __shared__ int wsum[K3_W];
-  extern __shared__ int keep_l[];  // [S*k] the surviving entries (with next_h only)
+  extern __shared__ int keep_l[];  // [S*k] the surviving entries, then [S] the sentences' ids (with next_h only)
+  int* const sid_l = keep_l + S * k;
   const int tid = threadIdx.x;
   const bool lead = blockIdx.x == 0;
   const int live = S_dev ? min(S, *S_dev) : S;  // sentences past it do not exist this step
+  // sid[s] (inside the array for every s < S) is read without waiting for the
+  // device count, so both loads are in flight together; an id is used (to
+  // index lengths) only below the count
   auto is_alive = [&](int e) {
     const int s = e / k;
-    return s < live && t < lengths[sid[s]] - 1;
+    const int id = s < S ? sid[s] : 0;
+    return s < live && t < lengths[id] - 1;
   };
+  if (next_h)  // the live sentences' ids, for the state gather
+    for (int s = tid; s < S; s += K3_T) sid_l[s] = sid[s];
   const int kept = compact_entries_pass(S * k, is_alive, [&](int o, int e) {
     if (lead) {
       keep[o] = e;
@@ -104,15 +111,21 @@ __global__ __launch_bounds__(K3_T) void standin_step(int S, const int32_t* __res
     }
   }
   if (next_h) {
-    __syncthreads();  // keep_l complete
-    // this workgroup's surviving rows: an even share of the S*k the launch was sized for
-    const int per = (S * k + (int)gridDim.x - 1) / (int)gridDim.x;
-    const int r0 = min((int)blockIdx.x * per, kept), r1 = min(r0 + per, kept);
-    for (int i = r0 * row_words + tid; i < r1 * row_words; i += K3_T) {
-      const int r = i / row_words, w = i - r * row_words;
-      const int e = keep_l[r];
-      const long long src = ((long long)sid[e / k] * T + t + 1) * k + e % k;
-      next_h[i] = table[src * row_words + w];
+    __syncthreads();  // keep_l and sid_l complete
+    // this workgroup's surviving rows: an even share of the S*k the launch was
+    // sized for among the workgroups past the first (which did the bookkeeping),
+    // or all of them when it is alone
+    const int G = (int)gridDim.x > 1 ? (int)gridDim.x - 1 : 1;
+    const int b = (int)gridDim.x > 1 ? (int)blockIdx.x - 1 : 0;
+    if (b >= 0) {
+      const int per = (S * k + G - 1) / G;
+      const int r0 = min(b * per, kept), r1 = min(r0 + per, kept);
+      for (int i = r0 * row_words + tid; i < r1 * row_words; i += K3_T) {
+        const int r = i / row_words, w = i - r * row_words;
+        const int e = keep_l[r];
+        const long long src = ((long long)sid_l[e / k] * T + t + 1) * k + e % k;
+        next_h[i] = table[src * row_words + w];
+      }
     }
   }
 }
@@ -143,8 +156,9 @@ hipError_t launch_standin_next_h(int n_max, const int32_t* n_dev, int k, int T, 
   return hipGetLastError();
 }
 
-// The fused gather keeps the surviving entries in LDS: at most this many.
-constexpr int kStandinFusedMax = 16384;
+// The fused gather keeps the surviving entries and the sentences' ids in LDS:
+// at most this many bytes of them.
+constexpr long long kStandinFusedLds = 64 * 1024;
 
 hipError_t launch_standin_step(int S, const int32_t* S_dev, int k, int t, const int32_t* sid, const int32_t* lengths,
                                const float* score, int32_t* keep, int32_t* counts, int32_t* new_off,
@@ -153,7 +167,7 @@ hipError_t launch_standin_step(int S, const int32_t* S_dev, int k, int t, const 
   const long long M = (long long)S * k;
   const bool v16 = (row_bytes % 16 == 0) && ((uintptr_t)table % 16 == 0) && ((uintptr_t)next_h % 16 == 0);
   const long long words = next_h ? (long long)(v16 ? row_bytes / 16 : row_bytes / 4) : 0;
-  if (next_h && (M > kStandinFusedMax || M * words > INT_MAX)) {
+  if (next_h && ((M + S + 1) * (long long)sizeof(int32_t) > kStandinFusedLds || M * words > INT_MAX)) {
     // too many entries for one workgroup's LDS: the bookkeeping, then the gather
     standin_step<uint32_t><<<dim3(1), dim3(K3_T), 0, st>>>(S, S_dev, k, t, sid, lengths, score, keep, counts, new_off,
                                                         prev_next, sid_next, alive, counts_host, nullptr, 0,
@@ -168,20 +182,21 @@ hipError_t launch_standin_step(int S, const int32_t* S_dev, int k, int t, const 
                                                         nullptr, 0);
     return hipGetLastError();
   }
-  // one workgroup per 32 KB of states (at most 256): each works out the scan
-  // again, which costs little next to its share of the copy
+  // one workgroup per 32 KB of states (at most 256) after the first, which does
+  // the bookkeeping: each works out the scan again, which costs little next to
+  // its share of the copy
   const long long bytes = M * (long long)row_bytes;
-  const int G = (int)std::min<long long>(std::max<long long>((bytes + (32 << 10) - 1) >> 15, 1), 256);
-  const size_t lds = (size_t)std::max<long long>(M, 1) * sizeof(int32_t);
+  const int G = 1 + (int)std::min<long long>((bytes + (32 << 10) - 1) >> 15, 255);
+  const size_t lds = (size_t)(M + S + 1) * sizeof(int32_t);
   if (lds > 48 * 1024) {
     static bool attr_set[2] = {false, false};  // the LDS ceiling, raised once per process and variant
     if (!attr_set[v16]) {
       const hipError_t e = v16 ? hipFuncSetAttribute(reinterpret_cast<const void*>(&standin_step<uint4>),
                                                      hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                     kStandinFusedMax * (int)sizeof(int32_t))
+                                                     (int)kStandinFusedLds)
                                : hipFuncSetAttribute(reinterpret_cast<const void*>(&standin_step<uint32_t>),
                                                      hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                     kStandinFusedMax * (int)sizeof(int32_t));
+                                                     (int)kStandinFusedLds);
       if (e != hipSuccess) return e;
       attr_set[v16] = true;
     }

@@ -117,7 +117,7 @@ def test_standin_step_matches_its_definition(kb, S, k, S_live, H, gather):
     # the fused step = the stand-in's EOS mask, the stable compaction of that
     # mask (np.flatnonzero), the sentence offsets and the gathers (scores,
     # sentence ids and, with gather, the next states: 16-byte rows at H = 8,
-    # 4-byte words at H = 5; one launch up to 16384 entries, two past it at
+    # 4-byte words at H = 5; one launch while entries and ids fit in 64 KB, two past it at
     # 2048 x 12); sentences past the device count are dropped without reading
     # their (stale) ids
     from paper_1805_09863_amd import binding as kbb
