@@ -302,7 +302,12 @@ static hipError_t launch_k2_nq(const K2Args& a, hipStream_t st) {
   const int rows_per = (a.N + a.S - 1) / a.S;
   const int W = (int)std::min<size_t>(std::min(K2_MAXW, std::max(1, rows_per)), (144 * 1024) / per_wave);
   const size_t lds = (size_t)K2_LS * sizeof(int2) + (size_t)W * per_wave;
-  return W <= 8 ? launch_k2_w<NQ, 512>(a, W, lds, st) : launch_k2_w<NQ, 1024>(a, W, lds, st);
+  // past 128 splits a row's lists take more than 16 KB, so at most 8 waves fit:
+  // only the 512-thread form is built for 3 and 4 lists per lane
+  if constexpr (NQ >= 3)
+    return launch_k2_w<NQ, 512>(a, W, lds, st);
+  else
+    return W <= 8 ? launch_k2_w<NQ, 512>(a, W, lds, st) : launch_k2_w<NQ, 1024>(a, W, lds, st);
 }
 
 // A vocabulary shard's partial lists hold shard-local words; this moves them

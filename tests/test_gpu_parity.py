@@ -50,6 +50,10 @@ SMALL = [
     ([10] * 5, 128, 20000, 6, "bf16"),         # 50 rows: two 32-row tiles, DMA pipeline
     ([16] * 4, 256, 30000, 16, "bf16"),        # 64 rows: two full 32-row tiles, k = 16
     ([13] * 7, 128, 8000, 5, "bf16"),          # 91 rows: one 128-row tile, DMA pipeline
+    # the merge's forms: sentences of more than 8 rows over 98 splits (1024 threads,
+    # 2 lists per lane); of 5 rows over 157 splits (512 threads, 3 lists per lane)
+    ([12, 9], 128, 25000, 5, "bf16"),
+    ([5, 5], 128, 40000, 5, "bf16"),
 ]
 
 
