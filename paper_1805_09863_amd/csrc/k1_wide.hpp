@@ -90,6 +90,13 @@ static_assert(WideGeom::BH * 4 * WideGeom::CAPH * 4 <= (WideGeom::WE + WideGeom:
 __device__ __forceinline__ void set_m0(uint32_t lds_base) {
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0" ::"s"(__builtin_amdgcn_readfirstlane(lds_base)) : "m0");
 }
+// A vector memory instruction that reads an SGPR needs 5 wait states after a
+// VALU instruction that wrote it (v_readfirstlane, or the v_readlane that
+// restores a spilled SGPR); the compiler inserts them for its own
+// instructions, not for inline assembly.  The build checks the device
+// assembly of this file for the hazard on every path (isa_check.py).  Here,
+// in the main loop, the base pair is a loop invariant that the compiler keeps
+// in SGPRs; load4_async below guards itself.
 template <int OFF>
 __device__ __forceinline__ void dma16_off(uint32_t voff, const void* sbase) {
   const uint64_t p = reinterpret_cast<uint64_t>(sbase);
@@ -126,13 +133,20 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ void atomic_umax_nowait(uint32_t* p, uint32_t v) {
   asm volatile("global_atomic_umax %0, %1, off" ::"v"(p), "v"(v) : "memory");
 }
-// 4-byte load from a wave-uniform base (SGPR pair) plus a per-lane byte offset
+// 4-byte load from a wave-uniform base (SGPR pair) plus a per-lane byte offset.
+// The base is first copied by a scalar move into a pair of the statement's
+// own (a scalar instruction waits for a VALU write by itself, and a scalar
+// write needs no wait states before the load): the loads run in the
+// epilogue, where register pressure can make the compiler spill the base
+// pair and restore it with v_readlane right before them (unguarded, builds
+// that did so read a stale base and faulted).
 __device__ __forceinline__ uint32_t load4_async(uint32_t voff, const void* sbase) {
   const uint64_t p = reinterpret_cast<uint64_t>(sbase);
   const uint64_t u = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(p >> 32)) << 32) |
                      (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)p);
   uint32_t v;
-  asm volatile("global_load_dword %0, %1, %2" : "=v"(v) : "v"(voff), "s"(reinterpret_cast<const void*>(u)));
+  uint64_t t;
+  asm volatile("s_mov_b64 %1, %3\n\tglobal_load_dword %0, %2, %1" : "=v"(v), "=&s"(t) : "v"(voff), "s"(u));
   return v;
 }
 // every vector memory operation of the wave done; the registers pass
