@@ -458,26 +458,33 @@ def sweep_bench(torch, np, kb):
         step.append({"N": N, "ms": ms, "hyps_per_s": N / (ms * 1e-3)})
         log(f"sweep step N={N}: {ms * 1e3:.1f} us")
     out["step_vs_rows"] = step
-    # (2) per-step time of the 1280-sentence decode
+    # (2) per-step time of the 1280-sentence decode: three timed runs after a
+    # warm-up, each step's median over them (a host that stalls between two
+    # steps of one run leaves the device idle, and that gap would count)
     curves = {}
     for compact in (True, False):
-        marks = []
-
-        def on_step(t, st, marks=marks):
-            e = torch.cuda.Event(enable_timing=True)
-            e.record()
-            marks.append((st["N"], e))
         decode_loop(h_table, W, b, L, p0, beam, T, compact=compact)          # warm-up
         torch.cuda.synchronize()
-        start = torch.cuda.Event(enable_timing=True)
-        start.record()
-        decode_loop(h_table, W, b, L, p0, beam, T, compact=compact, on_step=on_step)
-        torch.cuda.synchronize()
-        prev_e, per = start, []
-        for n, e in marks:
-            per.append({"rows": n, "ms": prev_e.elapsed_time(e)})
-            prev_e = e
-        curves["compacted" if compact else "naive"] = per
+        runs = []
+        for _ in range(3):
+            marks = []
+
+            def on_step(t, st, marks=marks):
+                e = torch.cuda.Event(enable_timing=True)
+                e.record()
+                marks.append((st["N"], e))
+            start = torch.cuda.Event(enable_timing=True)
+            start.record()
+            decode_loop(h_table, W, b, L, p0, beam, T, compact=compact, on_step=on_step)
+            torch.cuda.synchronize()
+            prev_e, per = start, []
+            for n, e in marks:
+                per.append((n, prev_e.elapsed_time(e)))
+                prev_e = e
+            runs.append(per)
+        curves["compacted" if compact else "naive"] = [
+            {"rows": runs[0][t][0], "ms": float(np.median([r[t][1] for r in runs])),
+             "ms_runs": [r[t][1] for r in runs]} for t in range(len(runs[0]))]
     out["per_step_1280"] = curves
     # (3) decode throughput against the number of sentences
     by_s = []
