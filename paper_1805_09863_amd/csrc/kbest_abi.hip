@@ -119,6 +119,34 @@ constexpr size_t kFewLdsMax = 160 * 1024;
 // slower from 6 rows, at V=90k (from one row: 47 against 41 us) and at
 // H=2048 (W of 88-102 M weights, where its bf16 dot products are the bound).
 constexpr long long kFewMaxWorkF32 = 1ll << 30;
+
+// Float32 tiles (register-staged, fp32 MFMA): a step takes about
+//   (a H + e) x (rows x words one workgroup covers) + f  microseconds,
+// the workgroup covering row_tile x word_tile x tiles-per-split.  a, e and f
+// per layout are fitted to the projection times of every layout measured at
+// H 256-2048, V 8k-60k and 40-1280 rows (k = 5); choosing the layout by this
+// model comes within 6% of the fastest measured one on each of those 120
+// shapes.  The 256-row x 128-word tile is left out: it fits the model poorly
+// and was fastest only by 3-6%, at 160 rows.
+struct F32Cost {
+  int layout, BH, BV;
+  double a, e, f;
+};
+constexpr F32Cost kF32Costs[4] = {
+    {kb::K1_L128, 128, 256, 4.905e-6, 4.269e-4, 14.67},
+    {kb::K1_L32, 32, 512, 6.798e-6, 3.311e-4, 19.61},
+    {kb::K1_L32M, 32, 256, 6.732e-6, 4.923e-4, 26.03},
+    {kb::K1_L32S, 32, 128, 8.102e-6, 3.343e-4, 24.71},
+};
+
+// splits of the vocabulary for a layout: one workgroup per CU over the row tiles
+int splits_for(int row_tiles, int n_vtiles) {
+  int P = kTargetCUs / (row_tiles > 0 ? row_tiles : 1);
+  if (P < 1) P = 1;
+  if (P > n_vtiles) P = n_vtiles;
+  if (P > 256) P = 256;
+  return P;
+}
 constexpr long long kFewMaxWorkBf16 = 200ll << 20;
 constexpr long long kFewMaxWeightsBf16 = 64ll << 20;
 
@@ -140,13 +168,24 @@ Plan make_plan(int dtype, int N, int H, int V, int k, bool dma, bool vec) {
     p.layout = kb::K1_W256;
     p.BH = 256;
     p.BV = 256;
+  } else if (dtype == KB_F32) {
+    double best = -1.0;
+    for (const F32Cost& c : kF32Costs) {
+      const int rt = (N + c.BH - 1) / c.BH, nt = (V + c.BV - 1) / c.BV;
+      const int P = splits_for(rt, nt), tps = (nt + P - 1) / P;
+      const double t = (c.a * H + c.e) * (double)c.BH * c.BV * tps + c.f;
+      if (best < 0.0 || t < best) {
+        best = t;
+        p.layout = c.layout;
+        p.BH = c.BH;
+        p.BV = c.BV;
+      }
+    }
   } else if (N > 192 && dtype == KB_BF16) {
     p.layout = kb::K1_L256;
     p.BH = 256;
     p.BV = 128;
   } else if (N >= (dma ? kDmaL128MinRows : 33)) {
-    // (float32 keeps this tile at every size: 9-10% faster than 128 words x
-    // 256 rows from 320 to 2048 rows, H=512, V=30k)
     p.layout = kb::K1_L128;
     p.BH = 128;
     p.BV = 256;
@@ -174,10 +213,7 @@ Plan make_plan(int dtype, int N, int H, int V, int k, bool dma, bool vec) {
   p.kc = k <= 4 ? 4 : (k <= 8 ? 8 : (k <= 12 ? 12 : 16));
   p.row_tiles = (N + p.BH - 1) / p.BH;
   p.n_vtiles = (V + p.BV - 1) / p.BV;
-  int P = kTargetCUs / (p.row_tiles > 0 ? p.row_tiles : 1);
-  if (P < 1) P = 1;
-  if (P > p.n_vtiles) P = p.n_vtiles;
-  if (P > 256) P = 256;
+  const int P = splits_for(p.row_tiles, p.n_vtiles);
   p.tps = (p.n_vtiles + P - 1) / P;
   p.P = (p.n_vtiles + p.tps - 1) / p.tps;  // no empty split
   p.stats_off = 0;

@@ -54,6 +54,13 @@ SMALL = [
     # 2 lists per lane); of 5 rows over 157 splits (512 threads, 3 lists per lane)
     ([12, 9], 128, 25000, 5, "bf16"),
     ([5, 5], 128, 40000, 5, "bf16"),
+    # float32 tiles as the planner's cost model picks them, each over two or
+    # more tiles per split with ragged rows and words
+    ([11, 11, 11], 64, 17004, 5, "f32"),       # 32 rows x 128 words
+    ([3] * 43, 64, 33004, 3, "f32"),           # 32 rows x 512 words
+    ([8] * 16 + [1], 256, 33004, 8, "f32"),    # 32 rows x 256 words, 3 tiles per split
+    ([7] * 23, 64, 65004, 7, "f32"),           # 128 rows x 256 words
+    ([23] * 7, 64, 65001, 12, "f32"),          # the same, V odd: scalar loads
 ]
 
 
