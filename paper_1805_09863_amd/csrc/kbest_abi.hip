@@ -96,13 +96,6 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // Splits whose running row maxima the 256 x 256 tile kernel shares (16 keys per row).
 constexpr int kGmaxSplits = 16;
 
-// Rows from which the 256 x 256 tile pays off (it needs the DMA pipeline):
-// measured against the 128 x 256, 256 x 128 and 512 x 32 tiles at 10-1024 rows
-// (V=50k, H=1024, k=5), it is the fastest from about 130 rows (e.g. 67 against
-// 92 us at 150 rows, 103 against 147 us at 320); below, the 256-word x 128-row
-// tile wins from 65 rows and 32-row tiles below that.
-constexpr int kWideMinRows = 129;
-constexpr int kDmaL128MinRows = 65;
 // The wide kernel's W source offsets assume at least one full 256-word tile.
 constexpr int kWideMinCols = 256;
 
@@ -120,23 +113,33 @@ constexpr size_t kFewLdsMax = 160 * 1024;
 // H=2048 (W of 88-102 M weights, where its bf16 dot products are the bound).
 constexpr long long kFewMaxWorkF32 = 1ll << 30;
 
-// Float32 tiles (register-staged, fp32 MFMA): a step takes about
+// Tile choice by a cost model.  A step's projection takes about
 //   (a H + e) x (rows x words one workgroup covers) + f  microseconds,
-// the workgroup covering row_tile x word_tile x tiles-per-split.  a, e and f
-// per layout are fitted to the projection times of every layout measured at
-// H 256-2048, V 8k-60k and 40-1280 rows (k = 5); choosing the layout by this
-// model comes within 6% of the fastest measured one on each of those 120
-// shapes.  The 256-row x 128-word tile is left out: it fits the model poorly
-// and was fastest only by 3-6%, at 160 rows.
-struct F32Cost {
+// the workgroup covering row tile x word tile x tiles per split.  a, e and f
+// per layout are fitted to the projection times of every layout forced in
+// turn (k = 5): float32 at H 256-2048, V 8k-60k and 40-1280 rows (120
+// shapes), bf16 on the DMA pipeline at H 512-2048, V 8k-90k and 40-2560 rows
+// (132 shapes).  Choosing by the model comes within 6% (float32) and 8%
+// (bf16) of the fastest measured layout on each shape.  For float32 the
+// 256-row x 128-word tile is left out: it fits the model poorly and was the
+// fastest only by 3-6%, at 160 rows.
+struct TileCost {
   int layout, BH, BV;
   double a, e, f;
 };
-constexpr F32Cost kF32Costs[4] = {
+constexpr TileCost kF32Costs[] = {
     {kb::K1_L128, 128, 256, 4.905e-6, 4.269e-4, 14.67},
     {kb::K1_L32, 32, 512, 6.798e-6, 3.311e-4, 19.61},
     {kb::K1_L32M, 32, 256, 6.732e-6, 4.923e-4, 26.03},
     {kb::K1_L32S, 32, 128, 8.102e-6, 3.343e-4, 24.71},
+};
+constexpr TileCost kBf16DmaCosts[] = {
+    {kb::K1_W256, 256, 256, 3.190e-7, 2.335e-4, 14.74},
+    {kb::K1_L128, 128, 256, 5.143e-7, 3.631e-4, 18.31},
+    {kb::K1_L256, 256, 128, 4.930e-7, 3.559e-4, 16.96},
+    {kb::K1_L32, 32, 512, 9.852e-7, 3.831e-4, 17.22},
+    {kb::K1_L32M, 32, 256, 1.263e-6, 5.146e-4, 20.39},
+    {kb::K1_L32S, 32, 128, 1.746e-6, 7.683e-4, 20.19},
 };
 
 // splits of the vocabulary for a layout: one workgroup per CU over the row tiles
@@ -146,6 +149,24 @@ int splits_for(int row_tiles, int n_vtiles) {
   if (P > n_vtiles) P = n_vtiles;
   if (P > 256) P = 256;
   return P;
+}
+
+// the layout of the least modelled time among n (ties keep the earlier)
+template <size_t n>
+void pick_by_model(const TileCost (&costs)[n], int N, int H, int V, Plan& p) {
+  double best = -1.0;
+  for (const TileCost& c : costs) {
+    if (c.layout == kb::K1_W256 && V < kWideMinCols) continue;
+    const int rt = (N + c.BH - 1) / c.BH, nt = (V + c.BV - 1) / c.BV;
+    const int P = splits_for(rt, nt), tps = (nt + P - 1) / P;
+    const double t = (c.a * H + c.e) * (double)c.BH * c.BV * tps + c.f;
+    if (best < 0.0 || t < best) {
+      best = t;
+      p.layout = c.layout;
+      p.BH = c.BH;
+      p.BV = c.BV;
+    }
+  }
 }
 constexpr long long kFewMaxWorkBf16 = 200ll << 20;
 constexpr long long kFewMaxWeightsBf16 = 64ll << 20;
@@ -164,33 +185,20 @@ Plan make_plan(int dtype, int N, int H, int V, int k, bool dma, bool vec) {
     p.layout = kb::K1_FEW;
     p.BH = kb::FEW_ROWS;
     p.BV = few_cw;
-  } else if (dma && N >= kWideMinRows && V >= kWideMinCols && dma_shape(dtype, H, V)) {
-    p.layout = kb::K1_W256;
-    p.BH = 256;
-    p.BV = 256;
+  } else if (dma && dma_shape(dtype, H, V)) {
+    pick_by_model(kBf16DmaCosts, N, H, V, p);
   } else if (dtype == KB_F32) {
-    double best = -1.0;
-    for (const F32Cost& c : kF32Costs) {
-      const int rt = (N + c.BH - 1) / c.BH, nt = (V + c.BV - 1) / c.BV;
-      const int P = splits_for(rt, nt), tps = (nt + P - 1) / P;
-      const double t = (c.a * H + c.e) * (double)c.BH * c.BV * tps + c.f;
-      if (best < 0.0 || t < best) {
-        best = t;
-        p.layout = c.layout;
-        p.BH = c.BH;
-        p.BV = c.BV;
-      }
-    }
+    pick_by_model(kF32Costs, N, H, V, p);
   } else if (N > 192 && dtype == KB_BF16) {
     p.layout = kb::K1_L256;
     p.BH = 256;
     p.BV = 128;
-  } else if (N >= (dma ? kDmaL128MinRows : 33)) {
+  } else if (N >= 33) {
     p.layout = kb::K1_L128;
     p.BH = 128;
     p.BV = 256;
   } else {
-    // 32-row tiles (one, or two on the DMA path): the word tile sets how many
+    // 32-row tiles: the word tile sets how many
     // CUs take part.  Of 512, 256 and 128 words, the one with the shortest
     // split (tiles per split x (tile width + a per-tile cost of about 64
     // words' worth)) wins; ties keep the wider tile.

@@ -34,26 +34,35 @@ SMALL = [
     ([2] * 40, 200, 2048, 5, "bf16"),          # H not a multiple of 64
     ([1] * 37, 33, 1003, 3, "bf16"),           # unaligned H and V: scalar loads
     ([5] * 60, 256, 3000, 5, "f32"),           # 300 rows: large-N tile
-    ([5] * 80, 512, 1000, 5, "bf16"),          # 400 rows
-    ([9] * 30, 128, 20000, 9, "bf16"),
+    ([5] * 80, 512, 1000, 5, "bf16"),          # 400 rows: 13 row tiles of 32 rows x 128 words
+    ([9] * 30, 128, 20000, 9, "bf16"),         # 270 rows: 3 row tiles of 128 rows x 256 words
     ([1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15, 16, 17], 64, 5000, 7, "f32"),
     ([40, 3], 64, 60000, 16, "bf16"),          # many splits per row, a sentence of 40 rows
     ([20, 17, 1], 64, 30000, 13, "f32"),       # sentences longer than one merge chunk
     # 9-64 rows (8 or fewer go to the few-row kernel, tests/test_gpu_few.py):
-    # the word tile (512, 256 or 128) follows the vocabulary size
+    # the tile, chosen by the planner's cost model, follows the vocabulary size
     ([5, 5], 256, 50000, 5, "bf16"),           # 256-word tiles, DMA pipeline
     ([3, 2, 4], 128, 20000, 4, "bf16"),        # 128-word tiles, DMA pipeline
-    ([2] * 10, 128, 40000, 12, "bf16"),        # 256-word tiles, k = 12
+    ([2] * 10, 128, 40000, 12, "bf16"),        # 512-word tiles, k = 12
     ([4, 4, 1], 64, 40000, 3, "f32"),          # 256-word tiles, register-staged f32
     ([16, 16], 128, 70000, 16, "bf16"),        # 512-word tiles, k = 16, 32 rows
     ([2, 3, 1, 3], 128, 20000, 2, "bf16"),     # k = 2: merge lanes staged in pairs
     ([10] * 5, 128, 20000, 6, "bf16"),         # 50 rows: two 32-row tiles, DMA pipeline
     ([16] * 4, 256, 30000, 16, "bf16"),        # 64 rows: two full 32-row tiles, k = 16
-    ([13] * 7, 128, 8000, 5, "bf16"),          # 91 rows: one 128-row tile, DMA pipeline
-    # the merge's forms: sentences of more than 8 rows over 98 splits (1024 threads,
-    # 2 lists per lane); of 5 rows over 157 splits (512 threads, 3 lists per lane)
-    ([12, 9], 128, 25000, 5, "bf16"),
-    ([5, 5], 128, 40000, 5, "bf16"),
+    ([13] * 7, 128, 8000, 5, "bf16"),          # 91 rows: three 32-row tiles of 128 words, DMA pipeline
+    # the merge's forms: sentences of more than 8 rows over 95 splits (1024 threads,
+    # 2 lists per lane); of 5 rows over 155 splits (512 threads, 3 lists per lane)
+    ([12, 9], 128, 12040, 5, "bf16"),
+    ([5, 5], 128, 19720, 5, "bf16"),
+    # each bf16 tile of the DMA pipeline as the cost model picks it, with ragged
+    # rows and words, over several row tiles or several tiles per split
+    ([43] * 6, 128, 22000, 12, "bf16"),        # 256 x 256, two row tiles
+    ([10] * 19 + [3], 128, 74000, 5, "bf16"),  # 256 x 256, two tiles per split
+    ([6] * 17, 128, 99000, 6, "bf16"),         # 128 rows x 256 words, two tiles per split
+    ([3] * 97, 128, 13000, 3, "bf16"),         # 256 rows x 128 words, two row tiles
+    ([11] * 3, 128, 66000, 11, "bf16"),        # 32 rows x 512 words, two row tiles, two tiles per split
+    ([3] * 11, 256, 17000, 3, "bf16"),         # 32 rows x 256 words, two row tiles
+    ([33], 128, 1000, 16, "bf16"),             # 32 rows x 128 words, two row tiles
     # float32 tiles as the planner's cost model picks them, each over two or
     # more tiles per split with ragged rows and words
     ([11, 11, 11], 64, 17004, 5, "f32"),       # 32 rows x 128 words
