@@ -84,6 +84,40 @@ const char* kb_last_error(void);
 size_t kb_kbest_workspace_bytes(int dtype, int N, int H, int V, int k, int S);
 
 /*
+ * The projection plan kb_kbest_step (and kb_argmax_step, kb_shard_partials)
+ * would choose for this shape when h, W and b have these addresses: which
+ * kernel and tile (Section 2.2's fused pass, Algorithm 4), and how the
+ * vocabulary is cut into splits (Algorithm 6).  Only the addresses'
+ * alignment matters: nothing is read through them and no device call is
+ * made, so any values will do (e.g. multiples of 16 for aligned operands).
+ * For tests, tuning and capacity planning.
+ *
+ *   plan_out  KB_PLAN_FIELDS int32, written on KB_OK (all 0 when N == 0):
+ *     [KB_PLAN_KERNEL]           one of KB_KERNEL_* below
+ *     [KB_PLAN_TILE_ROWS]        rows per tile (KB_KERNEL_FEW: rows it holds)
+ *     [KB_PLAN_TILE_WORDS]       words per tile (KB_KERNEL_FEW: per chunk)
+ *     [KB_PLAN_ROW_TILES]        ceil(N / rows per tile)
+ *     [KB_PLAN_SPLITS]           P, each split a run of whole tiles
+ *     [KB_PLAN_TILES_PER_SPLIT]  tiles in each split (the last may be short)
+ * Errors: the shape checks of kb_kbest_step (KB_ERR_INVALID_ARG,
+ * KB_ERR_UNSUPPORTED); KB_ERR_INVALID_ARG for a null plan_out or for h, W or
+ * b not aligned to their element size.
+ */
+#define KB_KERNEL_FEW 0  /* vector ALUs, W streamed once (a few rows)          */
+#define KB_KERNEL_WIDE 1 /* 256 x 256 tiles, matrix cores, LDS DMA pipeline   */
+#define KB_KERNEL_DMA 2  /* other tiles on the matrix cores, LDS DMA pipeline */
+#define KB_KERNEL_REG 3  /* matrix cores, operands staged through registers  */
+#define KB_PLAN_KERNEL 0
+#define KB_PLAN_TILE_ROWS 1
+#define KB_PLAN_TILE_WORDS 2
+#define KB_PLAN_ROW_TILES 3
+#define KB_PLAN_SPLITS 4
+#define KB_PLAN_TILES_PER_SPLIT 5
+#define KB_PLAN_FIELDS 6
+kb_status kb_kbest_plan(int dtype, int N, int H, int V, int k, const void* h, const void* W, const float* b,
+                        int32_t* plan_out);
+
+/*
  * kb_kbest_step -- one decode step of the output layer with the beam k-best.
  *
  * Computes, for every live hypothesis row n (Section 2.2 steps 1-3):

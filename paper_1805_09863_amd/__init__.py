@@ -8,5 +8,5 @@ this package only marshals arguments to it.
 """
 from .binding import (KB_BF16, KB_F32, KB_MAX_K, KBestError, abi_version, argmax_step,  # noqa: F401
                       argmax_workspace_bytes, compact_batch, compact_beams, compact_workspace_bytes, gather_rows, kbest_step, kbest_step_unfused,
-                      kbest_step_noalloc, kbest_workspace_bytes, lib, merge_partials, shard_partials, shard_splits,
+                      kbest_plan, kbest_step_noalloc, kbest_workspace_bytes, lib, merge_partials, shard_partials, shard_splits,
                       unfused_workspace_bytes, workspace)

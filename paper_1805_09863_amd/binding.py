@@ -31,6 +31,7 @@ SIGNATURES = {
     "kb_status_string": (ctypes.c_char_p, [_I]),
     "kb_last_error": (ctypes.c_char_p, []),
     "kb_kbest_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I, _I]),
+    "kb_kbest_plan": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _P]),
     "kb_kbest_step": (_I, [_I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "kb_kbest_step_events": (_I, [_I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P,
                                   _P, _P]),
@@ -162,6 +163,24 @@ def kbest_workspace_bytes(dtype: int, N: int, H: int, V: int, k: int, S: int) ->
     if n is None:
         n = _ws_bytes_cache[key] = int(L.kb_kbest_workspace_bytes(dtype, N, H, V, k, S))
     return n
+
+
+KB_KERNEL_NAMES = ("few", "wide", "dma", "reg")
+_PLAN_FIELDS = ("kernel", "tile_rows", "tile_words", "row_tiles", "splits", "tiles_per_split")
+
+
+def kbest_plan(dtype: int, N: int, H: int, V: int, k: int, aligned: bool = True) -> dict:
+    """The projection plan kbest_step chooses for this shape (kb_kbest_plan):
+    kernel ("few", "wide", "dma" or "reg"), tile rows and words, row tiles,
+    vocabulary splits and tiles per split.  ``aligned``: whether h, W and b
+    sit at 16-byte aligned addresses (torch allocations do)."""
+    esz = 2 if dtype == KB_BF16 else 4
+    base = 1 << 20 if aligned else (1 << 20) + esz
+    out = (ctypes.c_int32 * 6)()
+    _check(lib().kb_kbest_plan(dtype, N, H, V, k, base, base, (1 << 20) if aligned else (1 << 20) + 4, out))
+    plan = dict(zip(_PLAN_FIELDS, list(out)))
+    plan["kernel"] = KB_KERNEL_NAMES[plan["kernel"]] if N > 0 else None
+    return plan
 
 
 def workspace(nbytes: int, device=None) -> torch.Tensor:

@@ -453,6 +453,30 @@ const char* kb_status_string(kb_status s) {
 
 const char* kb_last_error(void) { return g_last_error.c_str(); }
 
+kb_status kb_kbest_plan(int dtype, int N, int H, int V, int k, const void* h, const void* W, const float* b,
+                        int32_t* plan_out) {
+  if (!plan_out) return fail(KB_ERR_INVALID_ARG, "plan_out is null");
+  kb_status st = validate_step(dtype, N, H, V, k, N > 0 ? 1 : 0);
+  if (st != KB_OK) return st;
+  for (int i = 0; i < KB_PLAN_FIELDS; ++i) plan_out[i] = 0;
+  if (N == 0) return ok();
+  const size_t esz = dtype == KB_BF16 ? 2 : 4;
+  if (!aligned(h, esz) || !aligned(W, esz) || !aligned(b, 4))
+    return fail(KB_ERR_INVALID_ARG, "h, W or b misaligned for its element type");
+  const bool vec = vec_operands(dtype, H, V, h, W);
+  const bool dma = dma_shape(dtype, H, V) && vec && aligned(b, 16);
+  const Plan p = make_plan(dtype, N, H, V, k, dma, vec);
+  plan_out[KB_PLAN_KERNEL] = p.layout == kb::K1_FEW ? KB_KERNEL_FEW
+                             : p.layout == kb::K1_W256 ? KB_KERNEL_WIDE
+                             : dma ? KB_KERNEL_DMA : KB_KERNEL_REG;
+  plan_out[KB_PLAN_TILE_ROWS] = p.BH;
+  plan_out[KB_PLAN_TILE_WORDS] = p.BV;
+  plan_out[KB_PLAN_ROW_TILES] = p.row_tiles;
+  plan_out[KB_PLAN_SPLITS] = p.P;
+  plan_out[KB_PLAN_TILES_PER_SPLIT] = p.tps;
+  return ok();
+}
+
 size_t kb_kbest_workspace_bytes(int dtype, int N, int H, int V, int k, int S) {
   if (validate_step(dtype, N, H, V, k, S) != KB_OK || N == 0) return 0;
   return workspace_bytes(dtype, N, H, V, k);

@@ -1,0 +1,75 @@
+"""Step shapes of the GPU parity tests, each with the projection plan it is
+meant to exercise ("kernel rows x words" per tile, as kb_kbest_plan reports
+it for 16-byte aligned operands).  tests/test_plan_cpu.py checks every plan
+on the CPU, so a planner change that moves a case off the kernel or tile it
+was written for fails there rather than silently testing something else."""
+
+SMALL = [
+    # (rows per sentence, H, V, k, dtype, plan) -- ragged tiles, tiny V, many splits
+    ([5], 256, 8000, 5, "f32", "few 8x64"),
+    ([1], 64, 33, 1, "f32", "reg 32x128"),             # V below one few-row chunk
+    ([3, 1, 4], 40, 517, 4, "f32", "reg 32x128"),      # H, V not multiples of the vector width
+    ([7, 2, 9, 1, 5], 96, 1500, 8, "bf16", "reg 32x128"),
+    ([12] * 6, 128, 4099, 12, "bf16", "reg 128x256"),
+    ([16] * 3, 64, 777, 16, "bf16", "reg 128x256"),
+    ([2] * 40, 200, 2048, 5, "bf16", "reg 128x256"),   # H not a multiple of 64
+    ([1] * 37, 33, 1003, 3, "bf16", "reg 128x256"),    # unaligned H and V: scalar loads
+    ([5] * 60, 256, 3000, 5, "f32", "reg 32x128"),     # 300 rows: ten 32-row tiles
+    ([5] * 80, 512, 1000, 5, "bf16", "dma 32x128"),    # 400 rows: 13 row tiles
+    ([9] * 30, 128, 20000, 9, "bf16", "dma 128x256"),  # 270 rows: 3 row tiles
+    ([1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15, 16, 17], 64, 5000, 7, "f32", "reg 32x128"),
+    ([40, 3], 64, 60000, 16, "bf16", "reg 128x256"),   # many splits per row, a sentence of 40 rows
+    ([20, 17, 1], 64, 30000, 13, "f32", "reg 32x128"),  # sentences longer than one merge chunk
+    # 9-64 rows (8 or fewer go to the few-row kernel, tests/test_gpu_few.py):
+    # the tile, chosen by the planner's cost model, follows the vocabulary size
+    ([5, 5], 256, 50000, 5, "bf16", "dma 32x256"),
+    ([3, 2, 4], 128, 20000, 4, "bf16", "dma 32x128"),
+    ([2] * 10, 128, 40000, 12, "bf16", "dma 32x512"),  # k = 12
+    ([4, 4, 1], 64, 40000, 3, "f32", "reg 32x128"),    # two tiles per split
+    ([16, 16], 128, 70000, 16, "bf16", "dma 32x512"),  # k = 16, 32 rows
+    ([2, 3, 1, 3], 128, 20000, 2, "bf16", "dma 32x128"),  # k = 2: merge lanes staged in pairs
+    ([10] * 5, 128, 20000, 6, "bf16", "dma 32x512"),   # 50 rows: two 32-row tiles
+    ([16] * 4, 256, 30000, 16, "bf16", "dma 32x256"),  # 64 rows: two full 32-row tiles, k = 16
+    ([13] * 7, 128, 8000, 5, "bf16", "dma 32x128"),    # 91 rows: three 32-row tiles
+    # the merge's forms: sentences of more than 8 rows over 95 splits (1024 threads,
+    # 2 lists per lane); of 5 rows over 155 splits (512 threads, 3 lists per lane)
+    ([12, 9], 128, 12040, 5, "bf16", "dma 32x128"),
+    ([5, 5], 128, 19720, 5, "bf16", "dma 32x128"),
+    # each bf16 tile of the DMA pipeline as the cost model picks it, with ragged
+    # rows and words, over several row tiles or several tiles per split
+    ([43] * 6, 128, 22000, 12, "bf16", "wide 256x256"),        # two row tiles
+    ([10] * 19 + [3], 128, 74000, 5, "bf16", "wide 256x256"),  # two tiles per split
+    ([6] * 17, 128, 99000, 6, "bf16", "dma 128x256"),          # two tiles per split
+    ([3] * 97, 128, 13000, 3, "bf16", "dma 256x128"),          # two row tiles
+    ([11] * 3, 128, 66000, 11, "bf16", "dma 32x512"),          # two row tiles, two tiles per split
+    ([3] * 11, 256, 17000, 3, "bf16", "dma 32x256"),           # two row tiles
+    ([33], 128, 1000, 16, "bf16", "dma 32x128"),               # two row tiles
+    # float32 tiles as the planner's cost model picks them, each over two or
+    # more tiles per split with ragged rows and words
+    ([11, 11, 11], 64, 17004, 5, "f32", "reg 32x128"),
+    ([3] * 43, 64, 33004, 3, "f32", "reg 32x512"),
+    ([8] * 16 + [1], 256, 33004, 8, "f32", "reg 32x256"),      # 3 tiles per split
+    ([7] * 23, 64, 65004, 7, "f32", "reg 128x256"),
+    ([23] * 7, 64, 65001, 12, "f32", "reg 128x256"),           # V odd: scalar loads
+]
+
+# The 256 x 256-tile projection kernel (bf16, H % 128 == 0, V % 8 == 0, and
+# a shape for which the planner's model picks it): ragged last row and word
+# tiles, a last word tile holding only 8 words, a short last split, 12 stages
+# per tile, one tile per split, k = 1 and k = 16, a single row tile mostly
+# padding.
+WIDE = [
+    # (rows per sentence, H, V, k, plan)
+    ([1] * 129, 128, 33000, 1, "wide 256x256"),              # 127 padding rows
+    ([5] * 40, 256, 33000, 5, "wide 256x256"),               # N 200
+    ([12] * 25 + [7], 128, 22000, 12, "wide 256x256"),       # N 307: two row tiles, the second ragged
+    ([4] * 128, 1024, 50000, 4, "wide 256x256"),             # N 512: two whole row tiles
+    ([5] * 120, 128, 26632, 5, "wide 256x256"),              # N 600; last word tile holds 8 words, alone in its split
+    ([12] * 50, 256, 26248, 12, "wide 256x256"),             # N 600; ragged word tile of 136, alone in its split
+    ([16] * 40, 384, 14000, 16, "wide 256x256"),             # k = 16, 12 stages per tile
+    ([1] * 700, 128, 11000, 1, "wide 256x256"),              # beam 1, k = 1
+    ([4] * 256, 1024, 30000, 4, "wide 256x256"),             # four whole row tiles, two tiles per split
+    ([3] * 250 + [2] * 20, 256, 10056, 8, "wide 256x256"),   # mixed beams, N 790
+    ([6] * 100, 128, 13312, 6, "wide 256x256"),              # one tile per split
+    ([5] * 120, 128, 200, 5, "dma 32x128"),                  # V < 256: no 256-word tile
+]

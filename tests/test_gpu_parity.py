@@ -10,6 +10,7 @@ import torch
 
 from synth import workloads as wl
 from tests.gpu_util import check, run_step, say, to_dev
+from tests.parity_cases import SMALL, WIDE
 
 pytestmark = pytest.mark.gpu
 
@@ -23,59 +24,9 @@ def kb():
     return kb
 
 
-SMALL = [
-    # (N rows per sentence, H, V, k, dtype)  -- ragged tiles, tiny V, many splits
-    ([5], 256, 8000, 5, "f32"),
-    ([1], 64, 33, 1, "f32"),
-    ([3, 1, 4], 40, 517, 4, "f32"),           # H, V not multiples of the vector width
-    ([7, 2, 9, 1, 5], 96, 1500, 8, "bf16"),
-    ([12] * 6, 128, 4099, 12, "bf16"),
-    ([16] * 3, 64, 777, 16, "bf16"),
-    ([2] * 40, 200, 2048, 5, "bf16"),          # H not a multiple of 64
-    ([1] * 37, 33, 1003, 3, "bf16"),           # unaligned H and V: scalar loads
-    ([5] * 60, 256, 3000, 5, "f32"),           # 300 rows: large-N tile
-    ([5] * 80, 512, 1000, 5, "bf16"),          # 400 rows: 13 row tiles of 32 rows x 128 words
-    ([9] * 30, 128, 20000, 9, "bf16"),         # 270 rows: 3 row tiles of 128 rows x 256 words
-    ([1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15, 16, 17], 64, 5000, 7, "f32"),
-    ([40, 3], 64, 60000, 16, "bf16"),          # many splits per row, a sentence of 40 rows
-    ([20, 17, 1], 64, 30000, 13, "f32"),       # sentences longer than one merge chunk
-    # 9-64 rows (8 or fewer go to the few-row kernel, tests/test_gpu_few.py):
-    # the tile, chosen by the planner's cost model, follows the vocabulary size
-    ([5, 5], 256, 50000, 5, "bf16"),           # 256-word tiles, DMA pipeline
-    ([3, 2, 4], 128, 20000, 4, "bf16"),        # 128-word tiles, DMA pipeline
-    ([2] * 10, 128, 40000, 12, "bf16"),        # 512-word tiles, k = 12
-    ([4, 4, 1], 64, 40000, 3, "f32"),          # 256-word tiles, register-staged f32
-    ([16, 16], 128, 70000, 16, "bf16"),        # 512-word tiles, k = 16, 32 rows
-    ([2, 3, 1, 3], 128, 20000, 2, "bf16"),     # k = 2: merge lanes staged in pairs
-    ([10] * 5, 128, 20000, 6, "bf16"),         # 50 rows: two 32-row tiles, DMA pipeline
-    ([16] * 4, 256, 30000, 16, "bf16"),        # 64 rows: two full 32-row tiles, k = 16
-    ([13] * 7, 128, 8000, 5, "bf16"),          # 91 rows: three 32-row tiles of 128 words, DMA pipeline
-    # the merge's forms: sentences of more than 8 rows over 95 splits (1024 threads,
-    # 2 lists per lane); of 5 rows over 155 splits (512 threads, 3 lists per lane)
-    ([12, 9], 128, 12040, 5, "bf16"),
-    ([5, 5], 128, 19720, 5, "bf16"),
-    # each bf16 tile of the DMA pipeline as the cost model picks it, with ragged
-    # rows and words, over several row tiles or several tiles per split
-    ([43] * 6, 128, 22000, 12, "bf16"),        # 256 x 256, two row tiles
-    ([10] * 19 + [3], 128, 74000, 5, "bf16"),  # 256 x 256, two tiles per split
-    ([6] * 17, 128, 99000, 6, "bf16"),         # 128 rows x 256 words, two tiles per split
-    ([3] * 97, 128, 13000, 3, "bf16"),         # 256 rows x 128 words, two row tiles
-    ([11] * 3, 128, 66000, 11, "bf16"),        # 32 rows x 512 words, two row tiles, two tiles per split
-    ([3] * 11, 256, 17000, 3, "bf16"),         # 32 rows x 256 words, two row tiles
-    ([33], 128, 1000, 16, "bf16"),             # 32 rows x 128 words, two row tiles
-    # float32 tiles as the planner's cost model picks them, each over two or
-    # more tiles per split with ragged rows and words
-    ([11, 11, 11], 64, 17004, 5, "f32"),       # 32 rows x 128 words
-    ([3] * 43, 64, 33004, 3, "f32"),           # 32 rows x 512 words
-    ([8] * 16 + [1], 256, 33004, 8, "f32"),    # 32 rows x 256 words, 3 tiles per split
-    ([7] * 23, 64, 65004, 7, "f32"),           # 128 rows x 256 words
-    ([23] * 7, 64, 65001, 12, "f32"),          # the same, V odd: scalar loads
-]
-
-
 @pytest.mark.parametrize("case", range(len(SMALL)))
 def test_small_shapes(kb, case):
-    rps, H, V, k, dt = SMALL[case]
+    rps, H, V, k, dt, _plan = SMALL[case]
     inp = wl.make_step(H=H, V=V, k=k, rows_per_sentence=rps, dtype=dt, seed=500 + case, name=f"small{case}")
     say(f"small case {case}: N={inp.N} H={H} V={V} k={k} {dt}")
     out = run_step(kb, inp, row_lse=True)
@@ -83,29 +34,9 @@ def test_small_shapes(kb, case):
     say(f"  max score err {rep.max_score_err:.2e}, {rep.n_checked_idx} exact ranks")
 
 
-# Shapes for the 256 x 256-tile projection kernel (bf16, H % 128 == 0,
-# V % 8 == 0, at least 129 rows): ragged last row and word tiles, a last
-# word tile holding only 8 words, the shortest state (4 stages per tile),
-# one tile per split, k = 1 and k = 16, a single row tile mostly padding.
-WIDE = [
-    ([1] * 129, 128, 3000, 1),                 # the fewest rows it takes: 127 padding rows
-    ([5] * 40, 256, 9000, 5),                  # N 200
-    ([12] * 25 + [7], 128, 5000, 12),          # N 307: two row tiles, the second ragged
-    ([4] * 128, 1024, 50000, 4),               # N 512: two whole row tiles
-    ([5] * 120, 128, 2056, 5),                 # N 600; last word tile holds 8 words
-    ([12] * 50, 256, 5000, 12),                # N 600; ragged word tile of 136
-    ([16] * 40, 384, 3000, 16),                # k = 16, 12 stages per tile
-    ([1] * 700, 128, 9000, 1),                 # beam 1, k = 1
-    ([4] * 256, 1024, 30000, 4),               # four whole row tiles
-    ([3] * 250 + [2] * 20, 256, 6216, 8),      # mixed beams, N 790
-    ([6] * 100, 128, 1024, 6),                 # 4 word tiles: one tile per split
-    ([5] * 120, 128, 200, 5),                  # V < 256: planned on the 256 x 128 tile
-]
-
-
 @pytest.mark.parametrize("case", range(len(WIDE)))
 def test_wide_tile_shapes(kb, case):
-    rps, H, V, k = WIDE[case]
+    rps, H, V, k, _plan = WIDE[case]
     inp = wl.make_step(H=H, V=V, k=k, rows_per_sentence=rps, dtype="bf16", seed=900 + case, name=f"wide{case}")
     say(f"wide case {case}: N={inp.N} H={H} V={V} k={k}")
     out = run_step(kb, inp, row_lse=True)
