@@ -73,3 +73,34 @@ WIDE = [
     ([6] * 100, 128, 13312, 6, "wide 256x256"),              # one tile per split
     ([5] * 120, 128, 200, 5, "dma 32x128"),                  # V < 256: no 256-word tile
 ]
+
+# Greedy steps (kb_argmax_step): every projection kernel, the 256 x 256 one in
+# its form without softmax statistics.
+ARGMAX = [
+    # (N, H, V, dtype, plan)
+    (5, 256, 8000, "f32", "few 8x64"),
+    (37, 33, 1003, "bf16", "reg 128x256"),       # unaligned H and V
+    (5, 256, 8000, "bf16", "few 8x128"),
+    (100, 128, 4099, "bf16", "reg 128x256"),     # V % 8 != 0: register-staged
+    (100, 128, 4096, "bf16", "dma 32x128"),      # four row tiles
+    (400, 512, 3000, "bf16", "dma 32x256"),
+    (600, 128, 2056, "bf16", "dma 32x512"),      # last word tile of 8
+    (600, 128, 26632, "bf16", "wide 256x256"),   # no statistics; last word tile of 8
+    (700, 256, 9000, "bf16", "dma 256x128"),
+    (1024, 1024, 30000, "bf16", "wide 256x256"),
+    (790, 384, 6216, "bf16", "dma 256x128"),
+    (65, 128, 44000, "bf16", "dma 128x256"),
+    (33, 128, 17000, "bf16", "dma 32x512"),      # two row tiles
+]
+
+# Vocabulary shards (Algorithm 6), each shard planned on its own words.
+SHARDS = [
+    # (rows per sentence, H, V, k, dtype, shard boundaries, plans of the shards)
+    ([12] * 25, 128, 44000, 12, "bf16", [0, 22000, 44000], {"wide 256x256"}),
+    ([12] * 50, 256, 5000, 12, "bf16", [0, 1256, 2504, 3752, 5000], {"dma 32x128"}),
+    ([5] * 8, 128, 3000, 5, "bf16", [0, 1000, 2000, 3000], {"dma 32x128"}),
+    ([3, 1, 4], 40, 517, 4, "f32", [0, 200, 517], {"few 8x64", "reg 32x128"}),   # ragged shards
+    ([16] * 3, 64, 4000, 16, "bf16", list(range(0, 4001, 500)), {"reg 128x256"}),  # 8 shards, k = 16
+    ([1] * 37, 33, 1003, 3, "bf16", [0, 333, 1003], {"reg 128x256"}),           # unaligned H and V
+    ([2, 7, 3], 128, 9000, 8, "bf16", [0, 8, 8992, 9000], {"dma 32x128"}),      # shards of 8 words beside a wide one
+]

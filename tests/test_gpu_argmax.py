@@ -4,10 +4,11 @@ oracle (Algorithm 5 per row), through the C ABI.
 Bar: the device logit within 1e-4 (float32) / 2e-2 (bf16) of the oracle's
 maximum; the token exact wherever the oracle's best and second-best scores
 differ by more than that, else the device token's oracle score within the
-tolerance of the maximum.  Covered: every projection kernel (register-staged
-float32, the DMA kernels at their three row tiles, the 256 x 256 tile without
-softmax statistics), ragged tiles, exact ties from duplicated columns, and
-the V=90k shape at 1280 rows (sampled rows).
+tolerance of the maximum.  Covered: every projection kernel (few-row,
+register-staged, the DMA kernels at their row tiles, the 256 x 256 tile
+without softmax statistics; the cases and their plans in
+tests/parity_cases.py), ragged tiles, exact ties from duplicated columns,
+and the V=90k shape at 1280 rows (sampled rows).
 """
 import numpy as np
 import pytest
@@ -16,6 +17,7 @@ import torch
 from oracle import kbest_oracle as ko
 from synth import workloads as wl
 from tests.gpu_util import TOL, say, to_dev
+from tests.parity_cases import ARGMAX
 
 pytestmark = pytest.mark.gpu
 
@@ -55,24 +57,11 @@ def _check(inp, tok, val, W=None, b=None, rows=None):
     return ref
 
 
-CASES = [
-    # (N, H, V, dtype)
-    (5, 256, 8000, "f32"),       # register-staged float32 kernel
-    (37, 33, 1003, "bf16"),      # unaligned H and V
-    (5, 256, 8000, "bf16"),      # DMA kernel, 32-row tile
-    (100, 128, 4099, "bf16"),    # DMA kernel, 128-row tile (V % 8 != 0: register-staged)
-    (100, 128, 4096, "bf16"),    # DMA kernel, 128-row tile
-    (400, 512, 3000, "bf16"),    # DMA kernel, 256-row tile
-    (600, 128, 2056, "bf16"),    # 256 x 256 tile without statistics; last word tile of 8
-    (700, 256, 9000, "bf16"),
-    (1024, 1024, 30000, "bf16"),
-    (790, 384, 6216, "bf16"),
-]
 
 
-@pytest.mark.parametrize("case", range(len(CASES)))
+@pytest.mark.parametrize("case", range(len(ARGMAX)))
 def test_argmax_shapes(kb, case):
-    N, H, V, dt = CASES[case]
+    N, H, V, dt, _plan = ARGMAX[case]
     inp = wl.make_step(H=H, V=V, k=1, S=N, beam=1, dtype=dt, seed=900 + case, name=f"argmax{case}")
     say(f"argmax case {case}: N={N} H={H} V={V} {dt}")
     h, W, b, _, _ = to_dev(inp)

@@ -11,6 +11,7 @@ import torch
 
 from synth import workloads as wl
 from tests.gpu_util import check, say, to_dev
+from tests.parity_cases import SHARDS
 
 pytestmark = pytest.mark.gpu
 
@@ -43,20 +44,11 @@ def run_sharded(kb, inp, cuts):
     return (tok.cpu().numpy(), par.cpu().numpy(), sc.cpu().numpy(), lse.cpu().numpy()), Ps
 
 
-CASES = [
-    # (rows per sentence, H, V, k, dtype, shard boundaries)
-    ([12] * 50, 256, 5000, 12, "bf16", [0, 1256, 2504, 3752, 5000]),   # 600 rows: 256 x 256 tiles in each shard
-    ([5] * 8, 128, 3000, 5, "bf16", [0, 1000, 2000, 3000]),             # 40 rows: DMA kernel, 128-row tiles
-    ([3, 1, 4], 40, 517, 4, "f32", [0, 200, 517]),                     # register-staged float32, ragged shards
-    ([16] * 3, 64, 4000, 16, "bf16", list(range(0, 4001, 500))),       # 8 shards, k = 16
-    ([1] * 37, 33, 1003, 3, "bf16", [0, 333, 1003]),                   # unaligned H and V: scalar loads
-    ([2, 7, 3], 128, 9000, 8, "bf16", [0, 8, 8992, 9000]),             # shards of 8 words beside a wide one
-]
 
 
-@pytest.mark.parametrize("case", range(len(CASES)))
+@pytest.mark.parametrize("case", range(len(SHARDS)))
 def test_shards_match_the_whole_vocabulary(kb, case):
-    rps, H, V, k, dt, cuts = CASES[case]
+    rps, H, V, k, dt, cuts, _plans = SHARDS[case]
     inp = wl.make_step(H=H, V=V, k=k, rows_per_sentence=rps, dtype=dt, seed=1700 + case, name=f"shards{case}")
     out, Ps = run_sharded(kb, inp, cuts)
     say(f"shards case {case}: N={inp.N} V={V} k={k} {dt}, {len(cuts) - 1} shards, splits {Ps}")

@@ -5,7 +5,7 @@ import pytest
 
 import paper_1805_09863_amd as kb
 from paper_1805_09863_amd.binding import KBestError
-from tests.parity_cases import SMALL, WIDE
+from tests.parity_cases import ARGMAX, SHARDS, SMALL, WIDE
 
 
 def _code(dt: str) -> int:
@@ -26,6 +26,19 @@ def test_small_case_plans(case):
 def test_wide_case_plans(case):
     rps, H, V, k, want = WIDE[case]
     assert _plan_str(kb.kbest_plan(kb.KB_BF16, sum(rps), H, V, k)) == want
+
+
+@pytest.mark.parametrize("case", range(len(ARGMAX)))
+def test_argmax_case_plans(case):
+    N, H, V, dt, want = ARGMAX[case]
+    assert _plan_str(kb.kbest_plan(_code(dt), N, H, V, 1)) == want
+
+
+@pytest.mark.parametrize("case", range(len(SHARDS)))
+def test_shard_case_plans(case):
+    rps, H, V, k, dt, cuts, want = SHARDS[case]
+    got = {_plan_str(kb.kbest_plan(_code(dt), sum(rps), H, b - a, k)) for a, b in zip(cuts, cuts[1:])}
+    assert got == want
 
 
 def test_wide_cases_keep_their_edges():
