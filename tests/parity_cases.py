@@ -104,3 +104,20 @@ SHARDS = [
     ([1] * 37, 33, 1003, 3, "bf16", [0, 333, 1003], {"reg 128x256"}),           # unaligned H and V
     ([2, 7, 3], 128, 9000, 8, "bf16", [0, 8, 8992, 9000], {"dma 32x128"}),      # shards of 8 words beside a wide one
 ]
+
+# Steps of at most 8 rows that the planner gives the few-row kernel (16-byte
+# loadable operands; W streamed once on the vector ALUs).
+FEW = [
+    # (rows per sentence, H, V, k, dtype, plan)
+    ([1], 256, 8000, 1, "f32", "few 8x64"),                # one row, k = 1
+    ([5], 256, 8000, 5, "bf16", "few 8x128"),
+    ([1], 1024, 60000, 16, "bf16", "few 8x128"),           # 2 chunks per split, k = 16
+    ([2, 2, 2, 2], 128, 60000, 12, "bf16", "few 8x128"),   # 2 chunks per split, four sentences
+    ([1] * 8, 128, 1000, 5, "f32", "few 8x64"),            # sentences of one row; last chunk 40 words
+    ([3], 64, 64, 3, "f32", "few 8x64"),                   # the vocabulary is one chunk
+    ([3], 2048, 9000, 5, "bf16", "few 8x128"),             # long states
+    ([7], 100, 5004, 4, "f32", "few 8x64"),                # H = 100: the last state slice is empty
+    ([6], 8, 3000, 6, "bf16", "few 8x128"),                # H = 8: only four state slices hold work
+    ([4, 3], 64, 136, 7, "bf16", "few 8x128"),             # 2 chunks, the second holds 8 words
+    ([2, 1], 256, 80000, 16, "f32", "few 8x64"),           # k = 16, 5 chunks per split of float32
+]

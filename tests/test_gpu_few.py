@@ -13,6 +13,7 @@ import torch
 
 from synth import workloads as wl
 from tests.gpu_util import check, run_step, say, to_dev
+from tests.parity_cases import FEW
 
 pytestmark = pytest.mark.gpu
 
@@ -26,25 +27,11 @@ def kb():
     return kb
 
 
-FEW = [
-    # (rows per sentence, H, V, k, dtype): shapes the planner gives the few-row kernel
-    ([1], 256, 8000, 1, "f32"),                 # one row, k = 1
-    ([5], 256, 8000, 5, "bf16"),
-    ([1], 1024, 60000, 16, "bf16"),             # 2 chunks per split, k = 16
-    ([2, 2, 2, 2], 128, 60000, 12, "bf16"),     # 2 chunks per split, four sentences
-    ([1] * 8, 128, 1000, 5, "f32"),             # sentences of one row; last chunk 40 words
-    ([3], 64, 64, 3, "f32"),                    # the vocabulary is one chunk
-    ([3], 2048, 9000, 5, "bf16"),               # long states
-    ([7], 100, 5004, 4, "f32"),                 # H = 100: the last state slice is empty
-    ([6], 8, 3000, 6, "bf16"),                  # H = 8: only four state slices hold work
-    ([4, 3], 64, 129, 7, "bf16"),               # 2 chunks, the second holds one word
-    ([2, 1], 256, 80000, 16, "f32"),            # k = 16, 5 chunks per split of float32
-]
 
 
 @pytest.mark.parametrize("case", range(len(FEW)))
 def test_few_rows(kb, case):
-    rps, H, V, k, dt = FEW[case]
+    rps, H, V, k, dt, _plan = FEW[case]
     inp = wl.make_step(H=H, V=V, k=k, rows_per_sentence=rps, dtype=dt, seed=1700 + case, name=f"few{case}")
     say(f"few-row case {case}: N={inp.N} H={H} V={V} k={k} {dt}")
     out = run_step(kb, inp, row_lse=True)

@@ -5,7 +5,7 @@ import pytest
 
 import paper_1805_09863_amd as kb
 from paper_1805_09863_amd.binding import KBestError
-from tests.parity_cases import ARGMAX, SHARDS, SMALL, WIDE
+from tests.parity_cases import ARGMAX, FEW, SHARDS, SMALL, WIDE
 
 
 def _code(dt: str) -> int:
@@ -26,6 +26,12 @@ def test_small_case_plans(case):
 def test_wide_case_plans(case):
     rps, H, V, k, want = WIDE[case]
     assert _plan_str(kb.kbest_plan(kb.KB_BF16, sum(rps), H, V, k)) == want
+
+
+@pytest.mark.parametrize("case", range(len(FEW)))
+def test_few_case_plans(case):
+    rps, H, V, k, dt, want = FEW[case]
+    assert _plan_str(kb.kbest_plan(_code(dt), sum(rps), H, V, k)) == want
 
 
 @pytest.mark.parametrize("case", range(len(ARGMAX)))
