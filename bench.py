@@ -45,34 +45,11 @@ def log(msg: str):
     print(msg, file=sys.stderr, flush=True)
 
 
-class HipEvents:
-    """Raw hipEvent_t handles from the HIP runtime torch already loaded."""
-
-    def __init__(self):
-        self.rt = ctypes.CDLL("libamdhip64.so.7")
-        self.rt.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
-        self.rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
-        self.rt.hipEventDestroy.argtypes = [ctypes.c_void_p]
-        self.rt.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
-
-    def create(self) -> int:
-        ev = ctypes.c_void_p()
-        if self.rt.hipEventCreate(ctypes.byref(ev)) != 0:
-            raise RuntimeError("hipEventCreate failed")
-        return ev.value
-
-    def elapsed_ms(self, a: int, b: int) -> float:
-        ms = ctypes.c_float()
-        if self.rt.hipEventElapsedTime(ctypes.byref(ms), ctypes.c_void_p(a), ctypes.c_void_p(b)) != 0:
-            raise RuntimeError("hipEventElapsedTime failed")
-        return float(ms.value)
-
-    def record(self, ev: int, stream: int):
-        if self.rt.hipEventRecord(ctypes.c_void_p(ev), ctypes.c_void_p(stream)) != 0:
-            raise RuntimeError("hipEventRecord failed")
-
-    def destroy(self, ev: int):
-        self.rt.hipEventDestroy(ctypes.c_void_p(ev))
+def HipEvents():
+    """Raw hipEvent_t handles (paper_1805_09863_amd/hipevents.py), imported
+    when first needed so that argument errors come before torch loads."""
+    from paper_1805_09863_amd.hipevents import HipEvents as _HipEvents
+    return _HipEvents()
 
 
 def k1_source_hash() -> str:

@@ -156,9 +156,10 @@ _ws_bytes_cache: dict = {}
 
 
 def kbest_workspace_bytes(dtype: int, N: int, H: int, V: int, k: int, S: int) -> int:
-    # a pure function of the shape (for one loaded library): asked once per shape
+    # a pure function of the shape (for one loaded library and tile override):
+    # asked once per shape
     L = lib()
-    key = (id(L), dtype, N, H, V, k, S)
+    key = (id(L), os.environ.get("KB_TILE"), dtype, N, H, V, k, S)
     n = _ws_bytes_cache.get(key)
     if n is None:
         n = _ws_bytes_cache[key] = int(L.kb_kbest_workspace_bytes(dtype, N, H, V, k, S))

@@ -116,11 +116,11 @@ constexpr long long kFewMaxWorkF32 = 1ll << 30;
 // Tile choice by a cost model.  A step's projection takes about
 //   (a H + e) x (rows x words one workgroup covers) + f  microseconds,
 // the workgroup covering row tile x word tile x tiles per split.  a, e and f
-// per layout are fitted to the projection times of every layout forced in
-// turn (k = 5): float32 at H 256-2048, V 8k-60k and 40-1280 rows (120
-// shapes), bf16 on the DMA pipeline at H 512-2048, V 8k-90k and 40-2560 rows
-// (132 shapes).  Choosing by the model comes within 6% (float32) and 8%
-// (bf16) of the fastest measured layout on each shape.  For float32 the
+// per layout are fitted by tune_planner.py to the projection times of every
+// layout forced in turn (KB_TILE; k = 5): float32 at H 256-2048, V 8k-60k and
+// 40-1280 rows (120 shapes), bf16 on the DMA pipeline at H 512-2048, V 8k-90k
+// and 40-2560 rows (132 shapes).  Choosing by the model comes within 6%
+// (float32) and 9% (bf16) of the fastest measured layout on each shape.  For float32 the
 // 256-row x 128-word tile is left out: it fits the model poorly and was the
 // fastest only by 3-6%, at 160 rows.
 struct TileCost {
@@ -128,18 +128,18 @@ struct TileCost {
   double a, e, f;
 };
 constexpr TileCost kF32Costs[] = {
-    {kb::K1_L128, 128, 256, 4.905e-6, 4.269e-4, 14.67},
-    {kb::K1_L32, 32, 512, 6.798e-6, 3.311e-4, 19.61},
-    {kb::K1_L32M, 32, 256, 6.732e-6, 4.923e-4, 26.03},
-    {kb::K1_L32S, 32, 128, 8.102e-6, 3.343e-4, 24.71},
+    {kb::K1_L128, 128, 256, 4.7971e-06, 5.1433e-04, 13.625},
+    {kb::K1_L32, 32, 512, 6.7494e-06, 4.2968e-04, 16.657},
+    {kb::K1_L32M, 32, 256, 6.7685e-06, 6.3867e-04, 18.986},
+    {kb::K1_L32S, 32, 128, 7.6774e-06, 8.7361e-04, 18.167},
 };
 constexpr TileCost kBf16DmaCosts[] = {
-    {kb::K1_W256, 256, 256, 3.190e-7, 2.335e-4, 14.74},
-    {kb::K1_L128, 128, 256, 5.143e-7, 3.631e-4, 18.31},
-    {kb::K1_L256, 256, 128, 4.930e-7, 3.559e-4, 16.96},
-    {kb::K1_L32, 32, 512, 9.852e-7, 3.831e-4, 17.22},
-    {kb::K1_L32M, 32, 256, 1.263e-6, 5.146e-4, 20.39},
-    {kb::K1_L32S, 32, 128, 1.746e-6, 7.683e-4, 20.19},
+    {kb::K1_W256, 256, 256, 3.2169e-07, 2.3262e-04, 14.720},
+    {kb::K1_L128, 128, 256, 5.1477e-07, 3.5748e-04, 18.414},
+    {kb::K1_L256, 256, 128, 4.8721e-07, 3.5373e-04, 17.299},
+    {kb::K1_L32, 32, 512, 9.8330e-07, 3.8379e-04, 17.150},
+    {kb::K1_L32M, 32, 256, 1.2663e-06, 5.1069e-04, 20.423},
+    {kb::K1_L32S, 32, 128, 1.7477e-06, 7.6189e-04, 20.280},
 };
 
 // splits of the vocabulary for a layout: one workgroup per CU over the row tiles
@@ -170,6 +170,29 @@ void pick_by_model(const TileCost (&costs)[n], int N, int H, int V, Plan& p) {
 }
 constexpr long long kFewMaxWorkBf16 = 200ll << 20;
 constexpr long long kFewMaxWeightsBf16 = 64ll << 20;
+
+// KB_TILE=<rows>x<words> (e.g. 32x256) at call time replaces the modelled
+// choice by that tile where the step's path has it (for measuring the cost
+// model; the tuning script sets it): on the DMA pipeline 256x256 (V >= 256),
+// 128x256, 256x128, 32x512, 32x256, 32x128; on the register-staged path the
+// same but 256x256.  Other values are ignored.
+void apply_tile_override(bool dma, int V, Plan& p) {
+  const char* e = getenv("KB_TILE");
+  int r = 0, w = 0;
+  char tail = 0;
+  if (e == nullptr || sscanf(e, "%dx%d%c", &r, &w, &tail) != 2) return;
+  int layout = -1;
+  if (r == 256 && w == 256 && dma && V >= kWideMinCols) layout = kb::K1_W256;
+  else if (r == 128 && w == 256) layout = kb::K1_L128;
+  else if (r == 256 && w == 128) layout = kb::K1_L256;
+  else if (r == 32 && w == 512) layout = kb::K1_L32;
+  else if (r == 32 && w == 256) layout = kb::K1_L32M;
+  else if (r == 32 && w == 128) layout = kb::K1_L32S;
+  if (layout < 0) return;
+  p.layout = layout;
+  p.BH = r;
+  p.BV = w;
+}
 
 Plan make_plan(int dtype, int N, int H, int V, int k, bool dma, bool vec) {
   Plan p{};
@@ -218,6 +241,7 @@ Plan make_plan(int dtype, int N, int H, int V, int k, bool dma, bool vec) {
     }
     p.BH = 32;
   }
+  if (p.layout != kb::K1_FEW) apply_tile_override(dma && dma_shape(dtype, H, V), V, p);
   p.kc = k <= 4 ? 4 : (k <= 8 ? 8 : (k <= 12 ? 12 : 16));
   p.row_tiles = (N + p.BH - 1) / p.BH;
   p.n_vtiles = (V + p.BV - 1) / p.BV;

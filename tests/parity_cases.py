@@ -19,13 +19,13 @@ SMALL = [
     ([9] * 30, 128, 20000, 9, "bf16", "dma 128x256"),  # 270 rows: 3 row tiles
     ([1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15, 16, 17], 64, 5000, 7, "f32", "reg 32x128"),
     ([40, 3], 64, 60000, 16, "bf16", "reg 128x256"),   # many splits per row, a sentence of 40 rows
-    ([20, 17, 1], 64, 30000, 13, "f32", "reg 32x128"),  # sentences longer than one merge chunk
+    ([20, 17, 1], 64, 30000, 13, "f32", "reg 32x256"),  # sentences longer than one merge chunk
     # 9-64 rows (8 or fewer go to the few-row kernel, tests/test_gpu_few.py):
     # the tile, chosen by the planner's cost model, follows the vocabulary size
     ([5, 5], 256, 50000, 5, "bf16", "dma 32x256"),
     ([3, 2, 4], 128, 20000, 4, "bf16", "dma 32x128"),
     ([2] * 10, 128, 40000, 12, "bf16", "dma 32x512"),  # k = 12
-    ([4, 4, 1], 64, 40000, 3, "f32", "reg 32x128"),    # two tiles per split
+    ([4, 4, 1], 64, 40000, 3, "f32", "reg 32x256"),
     ([16, 16], 128, 70000, 16, "bf16", "dma 32x512"),  # k = 16, 32 rows
     ([2, 3, 1, 3], 128, 20000, 2, "bf16", "dma 32x128"),  # k = 2: merge lanes staged in pairs
     ([10] * 5, 128, 20000, 6, "bf16", "dma 32x512"),   # 50 rows: two 32-row tiles
@@ -46,7 +46,7 @@ SMALL = [
     ([33], 128, 1000, 16, "bf16", "dma 32x128"),               # two row tiles
     # float32 tiles as the planner's cost model picks them, each over two or
     # more tiles per split with ragged rows and words
-    ([11, 11, 11], 64, 17004, 5, "f32", "reg 32x128"),
+    ([11, 11, 11], 256, 65540, 5, "f32", "reg 32x128"),      # 5 tiles per split
     ([3] * 43, 64, 33004, 3, "f32", "reg 32x512"),
     ([8] * 16 + [1], 256, 33004, 8, "f32", "reg 32x256"),      # 3 tiles per split
     ([7] * 23, 64, 65004, 7, "f32", "reg 128x256"),
