@@ -304,10 +304,22 @@ static hipError_t launch_k2_nq(const K2Args& a, hipStream_t st) {
   const size_t lds = (size_t)K2_LS * sizeof(int2) + (size_t)W * per_wave;
   // past 128 splits a row's lists take more than 16 KB, so at most 8 waves fit:
   // only the 512-thread form is built for 3 and 4 lists per lane
-  if constexpr (NQ >= 3)
+  if constexpr (NQ >= 3) {
     return launch_k2_w<NQ, 512>(a, W, lds, st);
-  else
-    return W <= 8 ? launch_k2_w<NQ, 512>(a, W, lds, st) : launch_k2_w<NQ, 1024>(a, W, lds, st);
+  } else {
+    // The 512-thread form stages a row's lists in batches of 32 loads per
+    // lane against 16, but takes about 210 VGPRs against 125: a CU then holds
+    // one workgroup of five waves instead of three.  It is used only where it
+    // saves a staging batch (a row's lists past 16 * 64 / kp splits, kp = k
+    // rounded up to a power of two) and the sentences need at most one
+    // workgroup per CU; with more (512 sentences at 25 splits, say) the
+    // 1024-thread form's occupancy halves the merge's time.
+    const int kp = a.k <= 1 ? 1 : (a.k <= 2 ? 2 : (a.k <= 4 ? 4 : (a.k <= 8 ? 8 : 16)));
+    const int per_batch = 16 * (64 / kp);  // lists of a row per batch of the 1024-thread form
+    const bool saves_batch = (a.P + per_batch - 1) / per_batch > (a.P + 2 * per_batch - 1) / (2 * per_batch);
+    return W <= 8 && saves_batch && a.S <= 256 ? launch_k2_w<NQ, 512>(a, W, lds, st)
+                                               : launch_k2_w<NQ, 1024>(a, W, lds, st);
+  }
 }
 
 // A vocabulary shard's partial lists hold shard-local words; this moves them
