@@ -38,9 +38,9 @@
  *  - The projection's tile is chosen by a cost model (kb_kbest_plan reports
  *    the choice).  With the environment variable KB_TILE=<rows>x<words> at
  *    call time (e.g. 32x256) a step not taken by the few-row kernel uses that
- *    tile instead where its path has it: with the DMA pipeline 256x256 (V >=
- *    256), 128x256, 256x128, 32x512, 32x256 or 32x128; register-staged the
- *    same but 256x256.  Other values are ignored.  It exists to measure the
+ *    tile instead where its path has it: 128x256, 256x128, 32x512, 32x256
+ *    or 32x128 on every path, and 256x256 on the bf16 DMA pipeline with
+ *    V >= 256.  Other values are ignored.  It exists to measure the
  *    model (paper_1805_09863_amd/tune_planner.py); the workspace size follows
  *    it, so size the workspace with the same setting.
  *  - Size limits (KB_ERR_UNSUPPORTED beyond them): N * V <= INT_MAX (a

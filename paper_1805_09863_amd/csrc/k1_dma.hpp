@@ -1,5 +1,6 @@
-// K1, DMA variant: the fused output-layer projection for bf16 h and W with
-// H % 128 == 0, V % 8 == 0 and 16-byte aligned operands (the production path).
+// K1, DMA variant: the fused output-layer projection for 16-byte aligned
+// operands, bf16 h and W with H % 128 == 0 and V % 8 == 0, or float32 with
+// H % 64 == 0 and V % 4 == 0.
 //
 // Same work split and epilogue as the register-staged kernel; the difference
 // is how operands reach the matrix cores.  A ring of NS LDS stages (BK = 32
@@ -12,22 +13,33 @@
 //   * h rows are stored row-major, 64 bytes (BK = 32 states) per row, with
 //     the four 16-byte chunks XOR-swizzled by row; one DMA instruction reads
 //     16 rows x 64 contiguous bytes, and B-fragment reads stay conflict-free.
+// Float32 (the fp32 MFMA 32x32x2): a stage holds BK = 16 states, the same
+// bytes per row of h (so the same h layout and swizzle) and 16 rows of W
+// stored as they arrive (a wave's A-fragment reads, 32 consecutive words of
+// one state per half-wave, need no swizzle).  Each lane takes its 16-byte
+// chunk of a row of h at once and feeds its 4 states to 4 consecutive
+// products: product step s of a stage pairs states 8 * (lane / 32) + s across
+// both operands, a fixed permutation of the stage's states, so the sums are
+// the same.
 // Each stage has its own __shared__ array, which lets the compiler see that
 // MFMA-side LDS reads never alias the DMA writes still in flight; the kernel
 // waits on the vector-memory counter itself (s_waitcnt vmcnt).
 #pragma once
 
+#include <type_traits>
+
 #include "k1_common.hpp"
 
 namespace kb {
 
-template <class L>
+template <class L, bool F32>
 struct DmaGeom {
-  static constexpr int BK = 32;                 // K per stage
+  static constexpr int BK = F32 ? 16 : 32;      // K per stage: 64 bytes of an h row
+  static constexpr int EPC = F32 ? 4 : 8;       // elements per 16-byte chunk
   static constexpr int NS = 4;                  // stages in the ring
-  static constexpr int WCH = L::BV / 8;         // 16-byte chunks per W row
+  static constexpr int WCH = L::BV / EPC;       // 16-byte chunks per W row
   static constexpr int W_SLOTS = BK * WCH;      // 16-byte chunks of W per stage
-  static constexpr int H_SLOTS = L::BH * BK / 8;
+  static constexpr int H_SLOTS = L::BH * 4;    // four 16-byte chunks per h row
   static constexpr int W_PER_WAVE = W_SLOTS / 4;
   static constexpr int H_PER_WAVE = H_SLOTS / 4;
   static constexpr int W_OPS = (W_PER_WAVE + 63) / 64;  // DMA instructions per wave per stage
@@ -37,12 +49,13 @@ struct DmaGeom {
   static_assert(W_PER_WAVE % 64 == 0 || W_PER_WAVE < 64, "whole or partial DMA instructions");
   static_assert(H_PER_WAVE % 64 == 0 || H_PER_WAVE < 64, "whole or partial DMA instructions");
   static_assert(WCH >= 16, "the swizzle permutes 16 chunks");
-  static_assert(BK == 32, "h rows hold four 16-byte chunks per stage");
+  static_assert(BK * (F32 ? 4 : 2) == 64, "h rows hold four 16-byte chunks per stage");
 };
 
-template <class L, int KC>
+template <class L, int KC, bool F32>
 struct DmaKernel {
-  using G = DmaGeom<L>;
+  using G = DmaGeom<L, F32>;
+  using E = typename std::conditional<F32, float, uint16_t>::type;
   static constexpr int BV = L::BV, BH = L::BH, WV = L::WV, WH = L::WH, NWV = L::NWV;
   static constexpr int BK = G::BK;
   // per-tile extras (bias, shared-threshold keys), issued with a tile's first stage
@@ -64,14 +77,14 @@ struct DmaKernel {
       const int s = wave * G::W_PER_WAVE + i * 64 + lane;
       const int r = s / G::WCH, pc = s % G::WCH;
       o.wr[i] = r;
-      o.wc[i] = (pc ^ wswz(r)) * 8;
+      o.wc[i] = (F32 ? pc : (pc ^ wswz(r))) * G::EPC;
     }
 #pragma unroll
     for (int i = 0; i < G::H_OPS; ++i) {
       // slot s = row * 4 + physical chunk; logical chunk = physical ^ hswz(row)
       const int s = wave * G::H_PER_WAVE + i * 64 + lane;
       const int n = s >> 2, pc = s & 3;
-      o.hoff[i] = min(h0 + n, a.N - 1) * a.H + (pc ^ hswz(n)) * 8;  // rows >= N: computed, never written
+      o.hoff[i] = min(h0 + n, a.N - 1) * a.H + (pc ^ hswz(n)) * G::EPC;  // rows >= N: computed, never written
     }
     o.trow = h0 + (wave * T_PER_WAVE + lane) * 4;  // 4 keys per 16 bytes; the key array is padded to whole row tiles
   }
@@ -82,14 +95,14 @@ struct DmaKernel {
                                                uint32_t bias_lds, uint32_t tgk_lds) {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const uint16_t* W = reinterpret_cast<const uint16_t*>(a.W) + (size_t)k0 * a.V;
-    const uint16_t* h = reinterpret_cast<const uint16_t*>(a.h) + k0;
+    const E* W = reinterpret_cast<const E*>(a.W) + (size_t)k0 * a.V;
+    const E* h = reinterpret_cast<const E*>(a.h) + k0;
     const bool ragged = v0 + BV > a.V;
 #pragma unroll
     for (int i = 0; i < G::W_OPS; ++i) {
       if (G::W_PER_WAVE >= 64 || lane < G::W_PER_WAVE) {
         int v = v0 + o.wc[i];
-        if (ragged) v = min(v, a.V - 8);  // words >= V are masked in the epilogue
+        if (ragged) v = min(v, a.V - G::EPC);  // words >= V are masked in the epilogue
         dma16(W + (size_t)o.wr[i] * a.V + v, sb + (wave * G::W_PER_WAVE + i * 64) * 16);
       }
     }
@@ -109,6 +122,10 @@ struct DmaKernel {
   }
 
   __device__ __forceinline__ static void compute(f32x16 (&acc)[WV][WH], const uint16_t* Wb, const uint16_t* Hb) {
+    if constexpr (F32) {
+      compute_f32(acc, reinterpret_cast<const float*>(Wb), reinterpret_cast<const float*>(Hb));
+      return;
+    }
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wv = wave % NWV, wh = wave / NWV;
     const int g = lane >> 4, j = lane & 15;
@@ -139,14 +156,46 @@ struct DmaKernel {
           acc[vb][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[vb], bf[hb], acc[vb][hb], 0, 0, 0);
     }
   }
+
+  // float32: step 4 c + s (c < 2, s < 4) of the stage pairs, in lane half g,
+  // state 8 g + 4 c + s: A (W, [state][word]) one float per lane, B (h)
+  // element s of the lane's 16-byte chunk 2 g + c of its row
+  __device__ __forceinline__ static void compute_f32(f32x16 (&acc)[WV][WH], const float* Wb, const float* Hb) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wv = wave % NWV, wh = wave / NWV;
+    const int g = lane >> 5, col = lane & 31;
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      float4 hq[WH];
+#pragma unroll
+      for (int hb = 0; hb < WH; ++hb) {
+        const int n = (wh * WH + hb) * 32 + col;
+        hq[hb] = *reinterpret_cast<const float4*>(Hb + (n * 4 + ((2 * g + c) ^ hswz(n))) * 4);
+      }
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const int kr = 8 * g + 4 * c + s;
+        float af[WV];
+#pragma unroll
+        for (int vb = 0; vb < WV; ++vb) af[vb] = Wb[kr * BV + (wv * WV + vb) * 32 + col];
+#pragma unroll
+        for (int vb = 0; vb < WV; ++vb)
+#pragma unroll
+          for (int hb = 0; hb < WH; ++hb) {
+            const float bv = s == 0 ? hq[hb].x : (s == 1 ? hq[hb].y : (s == 2 ? hq[hb].z : hq[hb].w));
+            acc[vb][hb] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[vb], bv, acc[vb][hb], 0, 0, 0);
+          }
+      }
+    }
+  }
 };
 
-template <class L, int KC>
+template <class L, int KC, bool F32>
 __global__ __launch_bounds__(256) void k1_dma(K1Args a) {
-  using D = DmaKernel<L, KC>;
-  using G = DmaGeom<L>;
+  using D = DmaKernel<L, KC, F32>;
+  using G = DmaGeom<L, F32>;
   constexpr int BV = L::BV, BH = L::BH, WV = L::WV, WH = L::WH, NWV = L::NWV;
-  constexpr int WE = G::W_SLOTS * 8, HE = G::H_SLOTS * 8;  // bf16 elements per stage
+  constexpr int WE = G::W_SLOTS * 8, HE = G::H_SLOTS * 8;  // 2-byte units per stage
   // one __shared__ object per stage: W, then h
   __shared__ __attribute__((aligned(16))) uint16_t S0[WE + HE], S1[WE + HE], S2[WE + HE], S3[WE + HE];
   __shared__ __attribute__((aligned(16))) SmemEpi<L> ep;
@@ -238,14 +287,14 @@ __global__ __launch_bounds__(256) void k1_dma(K1Args a) {
   epi.finish(ep, a, h0, split);
 }
 
-template <class L>
+template <class L, bool F32 = false>
 hipError_t launch_k1_dma_layout(int kc, dim3 grid, const K1Args& a, hipStream_t st) {
   const dim3 block(256);
   switch (kc) {
-    case 4: k1_dma<L, 4><<<grid, block, 0, st>>>(a); break;
-    case 8: k1_dma<L, 8><<<grid, block, 0, st>>>(a); break;
-    case 12: k1_dma<L, 12><<<grid, block, 0, st>>>(a); break;
-    case 16: k1_dma<L, 16><<<grid, block, 0, st>>>(a); break;
+    case 4: k1_dma<L, 4, F32><<<grid, block, 0, st>>>(a); break;
+    case 8: k1_dma<L, 8, F32><<<grid, block, 0, st>>>(a); break;
+    case 12: k1_dma<L, 12, F32><<<grid, block, 0, st>>>(a); break;
+    case 16: k1_dma<L, 16, F32><<<grid, block, 0, st>>>(a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -30,8 +30,23 @@ hipError_t launch_k1_reg_f32_L32S(int kc, dim3 grid, const K1Args& a, hipStream_
 hipError_t launch_k1_dma_L32M(int kc, dim3 grid, const K1Args& a, hipStream_t st);
 hipError_t launch_k1_dma_L32S(int kc, dim3 grid, const K1Args& a, hipStream_t st);
 hipError_t launch_k1_wide(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_dma_f32_L256(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_dma_f32_L128(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_dma_f32_L32(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_dma_f32_L32M(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_dma_f32_L32S(int kc, dim3 grid, const K1Args& a, hipStream_t st);
 
 hipError_t launch_k1(int bf16, int dma, int layout, int kc, dim3 grid, const K1Args& a, hipStream_t st) {
+  if (dma && !bf16) {
+    switch (layout) {
+      case K1_L256: return launch_k1_dma_f32_L256(kc, grid, a, st);
+      case K1_L128: return launch_k1_dma_f32_L128(kc, grid, a, st);
+      case K1_L32M: return launch_k1_dma_f32_L32M(kc, grid, a, st);
+      case K1_L32S: return launch_k1_dma_f32_L32S(kc, grid, a, st);
+      case K1_L32: return launch_k1_dma_f32_L32(kc, grid, a, st);
+      default: return hipErrorInvalidValue;  // the 256 x 256 tile is bf16 only
+    }
+  }
   if (dma) {
     switch (layout) {
       case K1_W256: return launch_k1_wide(kc, grid, a, st);
@@ -99,8 +114,12 @@ constexpr int kGmaxSplits = 16;
 // The wide kernel's W source offsets assume at least one full 256-word tile.
 constexpr int kWideMinCols = 256;
 
-// Shapes the DMA pipeline accepts, pointer alignment aside.
-bool dma_shape(int dtype, int H, int V) { return dtype == KB_BF16 && H % 128 == 0 && V % 8 == 0; }
+// Shapes the DMA pipeline accepts, pointer alignment aside: 64 bytes of an h
+// row per stage and whole 4-stage tiles (bf16 H % 128, float32 H % 64), W
+// rows of whole 16-byte chunks.
+bool dma_shape(int dtype, int H, int V) {
+  return dtype == KB_BF16 ? (H % 128 == 0 && V % 8 == 0) : (H % 64 == 0 && V % 4 == 0);
+}
 
 // The few-row kernel holds every row's state in LDS next to its partial sums.
 constexpr size_t kFewLdsMax = 160 * 1024;
@@ -117,12 +136,14 @@ constexpr long long kFewMaxWorkF32 = 1ll << 30;
 //   (a H + e) x (rows x words one workgroup covers) + f  microseconds,
 // the workgroup covering row tile x word tile x tiles per split.  a, e and f
 // per layout are fitted by tune_planner.py to the projection times of every
-// layout forced in turn (KB_TILE; k = 5): float32 at H 256-2048, V 8k-60k and
-// 40-1280 rows (120 shapes), bf16 on the DMA pipeline at H 512-2048, V 8k-90k
-// and 40-2560 rows (132 shapes).  Choosing by the model comes within 6%
-// (float32) and 9% (bf16) of the fastest measured layout on each shape.  For float32 the
-// 256-row x 128-word tile is left out: it fits the model poorly and was the
-// fastest only by 3-6%, at 160 rows.
+// layout forced in turn (KB_TILE; k = 5) over 40-1280 rows (bf16 2560), one
+// table per path: float32 register-staged and float32 on the DMA pipeline at
+// H 256-2048 (register-staged: measured while those shapes took that path;
+// now H not a multiple of 64), V 8k-60k (120 shapes each), bf16 on the DMA
+// pipeline at H 512-2048, V 8k-90k (132 shapes).  Choosing by the model comes
+// within 6%, 2% and 9% of the fastest measured layout on each shape.  For
+// register-staged float32 the 256-row x 128-word tile is left out: it fits
+// the model poorly and was the fastest only by 3-6%, at 160 rows.
 struct TileCost {
   int layout, BH, BV;
   double a, e, f;
@@ -140,6 +161,14 @@ constexpr TileCost kBf16DmaCosts[] = {
     {kb::K1_L32, 32, 512, 9.8330e-07, 3.8379e-04, 17.150},
     {kb::K1_L32M, 32, 256, 1.2663e-06, 5.1069e-04, 20.423},
     {kb::K1_L32S, 32, 128, 1.7477e-06, 7.6189e-04, 20.280},
+};
+// float32 on the DMA pipeline (fp32 MFMA, operands straight from LDS)
+constexpr TileCost kF32DmaCosts[] = {
+    {kb::K1_L128, 128, 256, 3.6741e-06, 4.5520e-04, 15.595},
+    {kb::K1_L256, 256, 128, 3.6795e-06, 4.3123e-04, 14.917},
+    {kb::K1_L32, 32, 512, 4.4655e-06, 5.0411e-04, 15.726},
+    {kb::K1_L32M, 32, 256, 4.9160e-06, 6.5679e-04, 19.436},
+    {kb::K1_L32S, 32, 128, 6.1006e-06, 9.3622e-04, 18.874},
 };
 
 // splits of the vocabulary for a layout: one workgroup per CU over the row tiles
@@ -173,16 +202,16 @@ constexpr long long kFewMaxWeightsBf16 = 64ll << 20;
 
 // KB_TILE=<rows>x<words> (e.g. 32x256) at call time replaces the modelled
 // choice by that tile where the step's path has it (for measuring the cost
-// model; the tuning script sets it): on the DMA pipeline 256x256 (V >= 256),
-// 128x256, 256x128, 32x512, 32x256, 32x128; on the register-staged path the
-// same but 256x256.  Other values are ignored.
-void apply_tile_override(bool dma, int V, Plan& p) {
+// model; the tuning script sets it): 128x256, 256x128, 32x512, 32x256,
+// 32x128, and 256x256 on the bf16 DMA pipeline with V >= 256 (wide_ok).
+// Other values are ignored.
+void apply_tile_override(bool wide_ok, Plan& p) {
   const char* e = getenv("KB_TILE");
   int r = 0, w = 0;
   char tail = 0;
   if (e == nullptr || sscanf(e, "%dx%d%c", &r, &w, &tail) != 2) return;
   int layout = -1;
-  if (r == 256 && w == 256 && dma && V >= kWideMinCols) layout = kb::K1_W256;
+  if (r == 256 && w == 256 && wide_ok) layout = kb::K1_W256;
   else if (r == 128 && w == 256) layout = kb::K1_L128;
   else if (r == 256 && w == 128) layout = kb::K1_L256;
   else if (r == 32 && w == 512) layout = kb::K1_L32;
@@ -209,7 +238,10 @@ Plan make_plan(int dtype, int N, int H, int V, int k, bool dma, bool vec) {
     p.BH = kb::FEW_ROWS;
     p.BV = few_cw;
   } else if (dma && dma_shape(dtype, H, V)) {
-    pick_by_model(kBf16DmaCosts, N, H, V, p);
+    if (dtype == KB_BF16)
+      pick_by_model(kBf16DmaCosts, N, H, V, p);
+    else
+      pick_by_model(kF32DmaCosts, N, H, V, p);
   } else if (dtype == KB_F32) {
     pick_by_model(kF32Costs, N, H, V, p);
   } else if (N > 192 && dtype == KB_BF16) {
@@ -241,7 +273,8 @@ Plan make_plan(int dtype, int N, int H, int V, int k, bool dma, bool vec) {
     }
     p.BH = 32;
   }
-  if (p.layout != kb::K1_FEW) apply_tile_override(dma && dma_shape(dtype, H, V), V, p);
+  if (p.layout != kb::K1_FEW)
+    apply_tile_override(dtype == KB_BF16 && dma && dma_shape(dtype, H, V) && V >= kWideMinCols, p);
   p.kc = k <= 4 ? 4 : (k <= 8 ? 8 : (k <= 12 ? 12 : 16));
   p.row_tiles = (N + p.BH - 1) / p.BH;
   p.n_vtiles = (V + p.BV - 1) / p.BV;
@@ -424,7 +457,7 @@ struct UfPlan {
   size_t logits_off, stats_off, lists_off, gthr_off, bytes;
 };
 
-bool uf_shape(int dtype, int H, int V) { return dma_shape(dtype, H, V) && V >= kWideMinCols; }
+bool uf_shape(int dtype, int H, int V) { return dtype == KB_BF16 && dma_shape(dtype, H, V) && V >= kWideMinCols; }
 
 UfPlan uf_plan(int N, int H, int V, int k) {
   UfPlan u{};

@@ -10,9 +10,12 @@ projection kernel of kbest_step is timed with HIP events on its own stream
 
 is fitted by least squares on relative error, and the choice the model
 makes on each shape is compared with the fastest tile measured there.  The
-constants of kF32Costs and kBf16DmaCosts in csrc/kbest_abi.hip come from this
-script's fit (H 256-2048 x V 8k-60k x 40-1,280 rows for float32, H 512-2048 x
-V 8k-90k x 40-2,560 rows for bf16, k = 5).
+constants of kF32DmaCosts, kF32Costs and kBf16DmaCosts in csrc/kbest_abi.hip
+come from this script's fit, one per path: --dtype f32 (H 256-2048, multiples
+of 64: the DMA pipeline), f32reg (H 264-2056: the register-staged kernel;
+kF32Costs was fitted at H 256-2048 while those shapes took it) and bf16 (the
+DMA pipeline, H 512-2048 x V 8k-90k x 40-2,560 rows); float32 over V 8k-60k x
+40-1,280 rows; k = 5.
 
     python -m paper_1805_09863_amd.tune_planner --dtype bf16 --out gpurun_out/tune_bf16.json
 
@@ -41,6 +44,9 @@ GRIDS = {
     "f32": dict(H=(256, 512, 1024, 2048), V=(8000, 30000, 60000),
                 N=(40, 64, 100, 160, 240, 320, 480, 640, 960, 1280),
                 tiles=("128x256", "256x128", "32x512", "32x256", "32x128")),
+    "f32reg": dict(H=(264, 520, 1032, 2056), V=(8000, 30000, 60000),
+                   N=(40, 64, 100, 160, 240, 320, 480, 640, 960, 1280),
+                   tiles=("128x256", "256x128", "32x512", "32x256", "32x128")),
     "bf16": dict(H=(512, 1024, 2048), V=(8000, 30000, 50000, 90000),
                  N=(40, 64, 100, 160, 240, 320, 480, 640, 960, 1280, 2560),
                  tiles=tuple(TILES)),
@@ -57,6 +63,7 @@ def workgroup_words(N: int, V: int, rows: int, words: int) -> int:
 def measure(dtype: str, grid: dict, reps: int, log) -> list:
     ev = HipEvents()
     code = binding.KB_BF16 if dtype == "bf16" else binding.KB_F32
+    want = {"bf16": ("wide", "dma"), "f32": ("dma",), "f32reg": ("reg",)}[dtype]
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     g = torch.Generator(device="cuda").manual_seed(7)
     rows = []
@@ -75,7 +82,7 @@ def measure(dtype: str, grid: dict, reps: int, log) -> list:
                 for tile in grid["tiles"]:
                     os.environ["KB_TILE"] = tile
                     plan = binding.kbest_plan(code, N, H, V, 5)
-                    if f"{plan['tile_rows']}x{plan['tile_words']}" != tile:
+                    if f"{plan['tile_rows']}x{plan['tile_words']}" != tile or plan["kernel"] not in want:
                         continue  # not on this path
                     ws = binding.workspace(binding.kbest_workspace_bytes(code, N, H, V, 5, S))
                     for _ in range(3):
@@ -140,7 +147,7 @@ def evaluate(rows: list, model: dict) -> dict:
 
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
-    ap.add_argument("--dtype", choices=("f32", "bf16"), required=True)
+    ap.add_argument("--dtype", choices=tuple(GRIDS), required=True)
     ap.add_argument("--reps", type=int, default=15)
     ap.add_argument("--out", required=True, help="JSON: measured times, fitted constants, evaluation")
     args = ap.parse_args()
@@ -150,8 +157,8 @@ def main():
     grid = GRIDS[args.dtype]
     rows = measure(args.dtype, grid, args.reps, log)
     model = fit(rows, grid["tiles"])
-    # the float32 planner leaves out the 256-row tile (it fits the model poorly)
-    used = {t: m for t, m in model.items() if not (args.dtype == "f32" and t == "256x128")}
+    # the register-staged float32 planner leaves out the 256-row tile (it fits the model poorly)
+    used = {t: m for t, m in model.items() if not (args.dtype == "f32reg" and t == "256x128")}
     res = {"dtype": args.dtype, "grid": {k: list(v) for k, v in grid.items()}, "rows": rows,
            "fit": model, "evaluation_of_the_planner_set": evaluate(rows, used)}
     with open(args.out, "w") as f:

@@ -14,18 +14,18 @@ SMALL = [
     ([16] * 3, 64, 777, 16, "bf16", "reg 128x256"),
     ([2] * 40, 200, 2048, 5, "bf16", "reg 128x256"),   # H not a multiple of 64
     ([1] * 37, 33, 1003, 3, "bf16", "reg 128x256"),    # unaligned H and V: scalar loads
-    ([5] * 60, 256, 3000, 5, "f32", "reg 32x128"),     # 300 rows: ten 32-row tiles
+    ([5] * 60, 256, 3000, 5, "f32", "dma 32x128"),     # 300 rows: ten 32-row tiles
     ([5] * 80, 512, 1000, 5, "bf16", "dma 32x128"),    # 400 rows: 13 row tiles
     ([9] * 30, 128, 20000, 9, "bf16", "dma 128x256"),  # 270 rows: 3 row tiles
-    ([1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15, 16, 17], 64, 5000, 7, "f32", "reg 32x128"),
+    ([1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15, 16, 17], 64, 5000, 7, "f32", "dma 32x128"),
     ([40, 3], 64, 60000, 16, "bf16", "reg 128x256"),   # many splits per row, a sentence of 40 rows
-    ([20, 17, 1], 64, 30000, 13, "f32", "reg 32x256"),  # sentences longer than one merge chunk
+    ([20, 17, 1], 64, 30000, 13, "f32", "dma 32x256"),  # sentences longer than one merge chunk
     # 9-64 rows (8 or fewer go to the few-row kernel, tests/test_gpu_few.py):
     # the tile, chosen by the planner's cost model, follows the vocabulary size
     ([5, 5], 256, 50000, 5, "bf16", "dma 32x256"),
     ([3, 2, 4], 128, 20000, 4, "bf16", "dma 32x128"),
     ([2] * 10, 128, 40000, 12, "bf16", "dma 32x512"),  # k = 12
-    ([4, 4, 1], 64, 40000, 3, "f32", "reg 32x256"),
+    ([4, 4, 1], 64, 40000, 3, "f32", "dma 32x256"),
     ([16, 16], 128, 70000, 16, "bf16", "dma 32x512"),  # k = 16, 32 rows
     ([2, 3, 1, 3], 128, 20000, 2, "bf16", "dma 32x128"),  # k = 2: merge lanes staged in pairs
     ([10] * 5, 128, 20000, 6, "bf16", "dma 32x512"),   # 50 rows: two 32-row tiles
@@ -44,12 +44,20 @@ SMALL = [
     ([11] * 3, 128, 66000, 11, "bf16", "dma 32x512"),          # two row tiles, two tiles per split
     ([3] * 11, 256, 17000, 3, "bf16", "dma 32x256"),           # two row tiles
     ([33], 128, 1000, 16, "bf16", "dma 32x128"),               # two row tiles
-    # float32 tiles as the planner's cost model picks them, each over two or
-    # more tiles per split with ragged rows and words
-    ([11, 11, 11], 256, 65540, 5, "f32", "reg 32x128"),      # 5 tiles per split
-    ([3] * 43, 64, 33004, 3, "f32", "reg 32x512"),
-    ([8] * 16 + [1], 256, 33004, 8, "f32", "reg 32x256"),      # 3 tiles per split
-    ([7] * 23, 64, 65004, 7, "f32", "reg 128x256"),
+    # float32 tiles as the planner's cost models pick them, each over two or
+    # more row tiles or tiles per split, with ragged rows and words: on the
+    # DMA pipeline (H % 64 == 0, V % 4 == 0) ...
+    ([11, 11, 11], 256, 65540, 5, "f32", "dma 32x256"),      # 3 tiles per split
+    ([3] * 43, 64, 33004, 3, "f32", "dma 32x512"),           # 5 row tiles, 2 tiles per split
+    ([8] * 16 + [1], 256, 33004, 8, "f32", "dma 32x256"),     # 3 tiles per split
+    ([7] * 23, 64, 65004, 7, "f32", "dma 256x128"),          # 2 tiles per split
+    ([8] * 65, 64, 13004, 8, "f32", "dma 128x256"),          # 5 row tiles
+    # ... and register-staged (H not a multiple of 64: 16-byte loads; V odd: scalar loads)
+    ([3] * 43, 96, 33004, 3, "f32", "reg 32x256"),           # 3 tiles per split
+    ([8] * 16 + [1], 288, 33004, 8, "f32", "reg 32x256"),
+    ([7] * 23, 96, 65004, 7, "f32", "reg 128x256"),          # 2 tiles per split
+    ([5] * 78, 96, 5004, 5, "f32", "reg 32x512"),            # 13 row tiles
+    ([20, 20], 96, 1004, 4, "f32", "reg 32x128"),            # two row tiles
     ([23] * 7, 64, 65001, 12, "f32", "reg 128x256"),           # V odd: scalar loads
 ]
 

@@ -12,12 +12,15 @@ pytestmark = pytest.mark.gpu
 
 DMA_TILES = ("256x256", "128x256", "256x128", "32x512", "32x256", "32x128")
 REG_TILES = ("128x256", "256x128", "32x512", "32x256", "32x128")
+F32_DMA_TILES = REG_TILES                           # the 256 x 256 tile is bf16 only
 STEPS = [
-    # (rows per sentence, H, V, k, dtype, tiles): DMA pipeline, then register-staged
+    # (rows per sentence, H, V, k, dtype, tiles): bf16 DMA pipeline, register-staged, float32 DMA
     ([7] * 43, 128, 5000, 7, "bf16", DMA_TILES),     # 301 rows, ragged words (5000 = 19 x 256 + 136)
     ([3] * 15, 256, 9000, 3, "bf16", DMA_TILES),     # 45 rows: a 256-row tile mostly padding
     ([7] * 43, 96, 5003, 7, "bf16", REG_TILES),      # H not a multiple of 128, V odd
-    ([5] * 61, 64, 4100, 5, "f32", REG_TILES),       # 305 rows
+    ([5] * 61, 96, 4100, 5, "f32", REG_TILES),       # 305 rows, H not a multiple of 64
+    ([5] * 61, 64, 4100, 5, "f32", F32_DMA_TILES),   # float32 DMA pipeline
+    ([3] * 15, 192, 9004, 3, "f32", F32_DMA_TILES),  # 45 rows, words 9004 = 35 x 256 + 44
 ]
 
 

@@ -69,7 +69,7 @@ def test_wide_cases_keep_their_edges():
 
 @pytest.mark.parametrize("dt,N,H,V,k,want", [
     ("f32", 5, 256, 8000, 5, ("few", 8, 64, 1, 125, 1)),              # one sentence, beam 5
-    ("f32", 320, 512, 30000, 5, ("reg", 32, 256, 10, 24, 5)),        # 64 sentences, beam 5
+    ("f32", 320, 512, 30000, 5, ("dma", 32, 256, 10, 24, 5)),        # 64 sentences, beam 5
     ("bf16", 640, 1024, 60000, 5, ("wide", 256, 256, 3, 79, 3)),     # 128 sentences, beam 5
     ("bf16", 3072, 1024, 90000, 12, ("wide", 256, 256, 12, 21, 17)),  # 256 sentences, beam 12
     ("bf16", 2560, 1024, 50000, 5, ("wide", 256, 256, 10, 25, 8)),   # the decode loop's first step
@@ -85,6 +85,11 @@ def test_plan_follows_alignment():
     assert kb.kbest_plan(kb.KB_BF16, 640, 1024, 60000, 5, aligned=False)["kernel"] == "reg"
     # nor can H that is not a multiple of 128
     assert kb.kbest_plan(kb.KB_BF16, 640, 1000, 60000, 5)["kernel"] == "reg"
+    # float32: H a multiple of 64 and V of 4, 16-byte aligned
+    assert kb.kbest_plan(kb.KB_F32, 320, 512, 30000, 5)["kernel"] == "dma"
+    assert kb.kbest_plan(kb.KB_F32, 320, 512, 30000, 5, aligned=False)["kernel"] == "reg"
+    assert kb.kbest_plan(kb.KB_F32, 320, 544, 30000, 5)["kernel"] == "reg"
+    assert kb.kbest_plan(kb.KB_F32, 320, 512, 30002, 5)["kernel"] == "reg"
 
 
 def test_plan_split_invariants():
