@@ -155,25 +155,31 @@ constexpr TileCost kF32Costs[] = {
     {kb::K1_L32S, 32, 128, 7.6774e-06, 8.7361e-04, 18.167},
 };
 constexpr TileCost kBf16DmaCosts[] = {
-    {kb::K1_W256, 256, 256, 3.2169e-07, 2.3262e-04, 14.720},
-    {kb::K1_L128, 128, 256, 5.1477e-07, 3.5748e-04, 18.414},
-    {kb::K1_L256, 256, 128, 4.8721e-07, 3.5373e-04, 17.299},
-    {kb::K1_L32, 32, 512, 9.8330e-07, 3.8379e-04, 17.150},
-    {kb::K1_L32M, 32, 256, 1.2663e-06, 5.1069e-04, 20.423},
-    {kb::K1_L32S, 32, 128, 1.7477e-06, 7.6189e-04, 20.280},
+    {kb::K1_W256, 256, 256, 3.1793e-07, 2.2198e-04, 15.664},
+    {kb::K1_L128, 128, 256, 5.0300e-07, 3.4708e-04, 19.122},
+    {kb::K1_L256, 256, 128, 4.8212e-07, 3.4390e-04, 17.873},
+    {kb::K1_L32, 32, 512, 9.7784e-07, 3.7621e-04, 17.473},
+    {kb::K1_L32M, 32, 256, 1.2656e-06, 5.0371e-04, 20.632},
+    {kb::K1_L32S, 32, 128, 2.7966e-06, 7.1836e-04, 15.656},
 };
 // float32 on the DMA pipeline (fp32 MFMA, operands straight from LDS)
 constexpr TileCost kF32DmaCosts[] = {
-    {kb::K1_L128, 128, 256, 3.6741e-06, 4.5520e-04, 15.595},
-    {kb::K1_L256, 256, 128, 3.6795e-06, 4.3123e-04, 14.917},
-    {kb::K1_L32, 32, 512, 4.4655e-06, 5.0411e-04, 15.726},
-    {kb::K1_L32M, 32, 256, 4.9160e-06, 6.5679e-04, 19.436},
-    {kb::K1_L32S, 32, 128, 6.1006e-06, 9.3622e-04, 18.874},
+    {kb::K1_L128, 128, 256, 3.6700e-06, 4.2906e-04, 15.920},
+    {kb::K1_L256, 256, 128, 3.6914e-06, 4.2281e-04, 14.781},
+    {kb::K1_L32, 32, 512, 4.4750e-06, 5.0180e-04, 15.731},
+    {kb::K1_L32M, 32, 256, 4.9317e-06, 6.5060e-04, 19.367},
+    {kb::K1_L32S, 32, 128, 8.7460e-06, 1.6116e-03, 12.312},
 };
 
-// splits of the vocabulary for a layout: one workgroup per CU over the row tiles
-int splits_for(int row_tiles, int n_vtiles) {
-  int P = kTargetCUs / (row_tiles > 0 ? row_tiles : 1);
+// Workgroups of a layout that one CU holds at once.  The DMA pipeline's
+// 32 x 128 tile takes 60 KB of LDS and at most 220 registers per lane, so two
+// run side by side and one's epilogue and barrier waits overlap the other's
+// products (its grid may reach 512 workgroups); every other tile fills a CU.
+int per_cu(int layout, bool dma) { return dma && layout == kb::K1_L32S ? 2 : 1; }
+
+// splits of the vocabulary for a layout: per_cu workgroups per CU over the row tiles
+int splits_for(int row_tiles, int n_vtiles, int per) {
+  int P = per * kTargetCUs / (row_tiles > 0 ? row_tiles : 1);
   if (P < 1) P = 1;
   if (P > n_vtiles) P = n_vtiles;
   if (P > 256) P = 256;
@@ -182,12 +188,12 @@ int splits_for(int row_tiles, int n_vtiles) {
 
 // the layout of the least modelled time among n (ties keep the earlier)
 template <size_t n>
-void pick_by_model(const TileCost (&costs)[n], int N, int H, int V, Plan& p) {
+void pick_by_model(const TileCost (&costs)[n], int N, int H, int V, bool dma, Plan& p) {
   double best = -1.0;
   for (const TileCost& c : costs) {
     if (c.layout == kb::K1_W256 && V < kWideMinCols) continue;
     const int rt = (N + c.BH - 1) / c.BH, nt = (V + c.BV - 1) / c.BV;
-    const int P = splits_for(rt, nt), tps = (nt + P - 1) / P;
+    const int P = splits_for(rt, nt, per_cu(c.layout, dma)), tps = (nt + P - 1) / P;
     const double t = (c.a * H + c.e) * (double)c.BH * c.BV * tps + c.f;
     if (best < 0.0 || t < best) {
       best = t;
@@ -239,11 +245,11 @@ Plan make_plan(int dtype, int N, int H, int V, int k, bool dma, bool vec) {
     p.BV = few_cw;
   } else if (dma && dma_shape(dtype, H, V)) {
     if (dtype == KB_BF16)
-      pick_by_model(kBf16DmaCosts, N, H, V, p);
+      pick_by_model(kBf16DmaCosts, N, H, V, true, p);
     else
-      pick_by_model(kF32DmaCosts, N, H, V, p);
+      pick_by_model(kF32DmaCosts, N, H, V, true, p);
   } else if (dtype == KB_F32) {
-    pick_by_model(kF32Costs, N, H, V, p);
+    pick_by_model(kF32Costs, N, H, V, false, p);
   } else if (N > 192 && dtype == KB_BF16) {
     p.layout = kb::K1_L256;
     p.BH = 256;
@@ -278,7 +284,7 @@ Plan make_plan(int dtype, int N, int H, int V, int k, bool dma, bool vec) {
   p.kc = k <= 4 ? 4 : (k <= 8 ? 8 : (k <= 12 ? 12 : 16));
   p.row_tiles = (N + p.BH - 1) / p.BH;
   p.n_vtiles = (V + p.BV - 1) / p.BV;
-  const int P = splits_for(p.row_tiles, p.n_vtiles);
+  const int P = splits_for(p.row_tiles, p.n_vtiles, per_cu(p.layout, dma && dma_shape(dtype, H, V)));
   p.tps = (p.n_vtiles + P - 1) / P;
   p.P = (p.n_vtiles + p.tps - 1) / p.tps;  // no empty split
   p.stats_off = 0;

@@ -53,10 +53,16 @@ GRIDS = {
 }
 
 
-def workgroup_words(N: int, V: int, rows: int, words: int) -> int:
+def per_cu(dtype, tile: str) -> int:
+    """Workgroups one CU holds at once, as the planner counts them: two of the
+    DMA pipeline's 32 x 128 tile, one of every other."""
+    return 2 if dtype in ("f32", "bf16") and tile == "32x128" else 1
+
+
+def workgroup_words(N: int, V: int, rows: int, words: int, per: int = 1) -> int:
     """rows x words one workgroup covers, with the planner's split rule."""
     rt, nt = -(-N // rows), -(-V // words)
-    P = max(1, min(256 // rt, nt, 256))
+    P = max(1, min(per * 256 // rt, nt, 256))
     return rows * words * -(-nt // P)
 
 
@@ -106,7 +112,7 @@ def measure(dtype: str, grid: dict, reps: int, log) -> list:
     return rows
 
 
-def fit(rows: list, tiles) -> dict:
+def fit(rows: list, tiles, dtype=None) -> dict:
     """(a, e, f) per tile: least squares on relative error."""
     out = {}
     for tile in tiles:
@@ -114,7 +120,8 @@ def fit(rows: list, tiles) -> dict:
         pts = [x for x in rows if tile in x["us"]]
         if len(pts) < 3:
             continue
-        X = np.array([[x["H"] * workgroup_words(x["N"], x["V"], r, w), workgroup_words(x["N"], x["V"], r, w), 1.0]
+        pc = per_cu(dtype, tile)
+        X = np.array([[x["H"] * workgroup_words(x["N"], x["V"], r, w, pc), workgroup_words(x["N"], x["V"], r, w, pc), 1.0]
                       for x in pts])
         y = np.array([x["us"][tile] for x in pts])
         c, *_ = np.linalg.lstsq(X / y[:, None], np.ones_like(y), rcond=None)
@@ -124,7 +131,7 @@ def fit(rows: list, tiles) -> dict:
     return out
 
 
-def evaluate(rows: list, model: dict) -> dict:
+def evaluate(rows: list, model: dict, dtype=None) -> dict:
     """The model's choice on each shape against the fastest tile measured."""
     worst, tot_choice, tot_best = 1.0, 0.0, 0.0
     for x in rows:
@@ -134,7 +141,7 @@ def evaluate(rows: list, model: dict) -> dict:
 
         def pred(t):
             r, w = TILES[t]
-            wg = workgroup_words(x["N"], x["V"], r, w)
+            wg = workgroup_words(x["N"], x["V"], r, w, per_cu(dtype, t))
             m = model[t]
             return (m["a"] * x["H"] + m["e"]) * wg + m["f"]
         choice = min(cands, key=pred)
@@ -156,11 +163,11 @@ def main():
         print(msg, file=sys.stderr, flush=True)
     grid = GRIDS[args.dtype]
     rows = measure(args.dtype, grid, args.reps, log)
-    model = fit(rows, grid["tiles"])
+    model = fit(rows, grid["tiles"], args.dtype)
     # the register-staged float32 planner leaves out the 256-row tile (it fits the model poorly)
     used = {t: m for t, m in model.items() if not (args.dtype == "f32reg" and t == "256x128")}
     res = {"dtype": args.dtype, "grid": {k: list(v) for k, v in grid.items()}, "rows": rows,
-           "fit": model, "evaluation_of_the_planner_set": evaluate(rows, used)}
+           "fit": model, "evaluation_of_the_planner_set": evaluate(rows, used, args.dtype)}
     with open(args.out, "w") as f:
         json.dump(res, f)
     for t, m in model.items():

@@ -1,8 +1,24 @@
 """Step shapes of the GPU parity tests, each with the projection plan it is
 meant to exercise ("kernel rows x words" per tile, as kb_kbest_plan reports
-it for 16-byte aligned operands).  tests/test_plan_cpu.py checks every plan
-on the CPU, so a planner change that moves a case off the kernel or tile it
-was written for fails there rather than silently testing something else."""
+it for 16-byte aligned operands).  The GPU tests pin each case's tile with
+KB_TILE (tile_env below), so a change of the cost models does not move a case
+off its kernel; tests/test_plan_cpu.py checks on the CPU that every case, so
+pinned, gets the kernel and tile it was written for (the kernel follows from
+dtype, alignment and the DMA shape rules, the few-row kernel from the row
+count).  Comments that say a tile is the model's pick held when the case was
+written."""
+
+
+def tile_env(monkeypatch, plans):
+    """Pin the tile of a plan string (or of the one non-few plan of a set) with
+    KB_TILE for the test's duration; few-row plans need no pinning."""
+    plans = [plans] if isinstance(plans, str) else sorted(plans)
+    tiles = {p.split()[1] for p in plans if not p.startswith("few ")}
+    assert len(tiles) <= 1, plans
+    if tiles:
+        monkeypatch.setenv("KB_TILE", tiles.pop())
+    else:
+        monkeypatch.delenv("KB_TILE", raising=False)
 
 SMALL = [
     # (rows per sentence, H, V, k, dtype, plan) -- ragged tiles, tiny V, many splits

@@ -17,7 +17,7 @@ import torch
 from oracle import kbest_oracle as ko
 from synth import workloads as wl
 from tests.gpu_util import TOL, say, to_dev
-from tests.parity_cases import ARGMAX
+from tests.parity_cases import ARGMAX, tile_env
 
 pytestmark = pytest.mark.gpu
 
@@ -60,8 +60,9 @@ def _check(inp, tok, val, W=None, b=None, rows=None):
 
 
 @pytest.mark.parametrize("case", range(len(ARGMAX)))
-def test_argmax_shapes(kb, case):
-    N, H, V, dt, _plan = ARGMAX[case]
+def test_argmax_shapes(kb, case, monkeypatch):
+    N, H, V, dt, plan = ARGMAX[case]
+    tile_env(monkeypatch, plan)
     inp = wl.make_step(H=H, V=V, k=1, S=N, beam=1, dtype=dt, seed=900 + case, name=f"argmax{case}")
     say(f"argmax case {case}: N={N} H={H} V={V} {dt}")
     h, W, b, _, _ = to_dev(inp)

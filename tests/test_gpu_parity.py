@@ -10,7 +10,7 @@ import torch
 
 from synth import workloads as wl
 from tests.gpu_util import check, run_step, say, to_dev
-from tests.parity_cases import SMALL, WIDE
+from tests.parity_cases import SMALL, WIDE, tile_env
 
 pytestmark = pytest.mark.gpu
 
@@ -25,8 +25,9 @@ def kb():
 
 
 @pytest.mark.parametrize("case", range(len(SMALL)))
-def test_small_shapes(kb, case):
-    rps, H, V, k, dt, _plan = SMALL[case]
+def test_small_shapes(kb, case, monkeypatch):
+    rps, H, V, k, dt, plan = SMALL[case]
+    tile_env(monkeypatch, plan)
     inp = wl.make_step(H=H, V=V, k=k, rows_per_sentence=rps, dtype=dt, seed=500 + case, name=f"small{case}")
     say(f"small case {case}: N={inp.N} H={H} V={V} k={k} {dt}")
     out = run_step(kb, inp, row_lse=True)
@@ -35,8 +36,9 @@ def test_small_shapes(kb, case):
 
 
 @pytest.mark.parametrize("case", range(len(WIDE)))
-def test_wide_tile_shapes(kb, case):
-    rps, H, V, k, _plan = WIDE[case]
+def test_wide_tile_shapes(kb, case, monkeypatch):
+    rps, H, V, k, plan = WIDE[case]
+    tile_env(monkeypatch, plan)
     inp = wl.make_step(H=H, V=V, k=k, rows_per_sentence=rps, dtype="bf16", seed=900 + case, name=f"wide{case}")
     say(f"wide case {case}: N={inp.N} H={H} V={V} k={k}")
     out = run_step(kb, inp, row_lse=True)

@@ -11,7 +11,7 @@ import torch
 
 from synth import workloads as wl
 from tests.gpu_util import check, say, to_dev
-from tests.parity_cases import SHARDS
+from tests.parity_cases import SHARDS, tile_env
 
 pytestmark = pytest.mark.gpu
 
@@ -47,8 +47,9 @@ def run_sharded(kb, inp, cuts):
 
 
 @pytest.mark.parametrize("case", range(len(SHARDS)))
-def test_shards_match_the_whole_vocabulary(kb, case):
-    rps, H, V, k, dt, cuts, _plans = SHARDS[case]
+def test_shards_match_the_whole_vocabulary(kb, case, monkeypatch):
+    rps, H, V, k, dt, cuts, plans = SHARDS[case]
+    tile_env(monkeypatch, plans)
     inp = wl.make_step(H=H, V=V, k=k, rows_per_sentence=rps, dtype=dt, seed=1700 + case, name=f"shards{case}")
     out, Ps = run_sharded(kb, inp, cuts)
     say(f"shards case {case}: N={inp.N} V={V} k={k} {dt}, {len(cuts) - 1} shards, splits {Ps}")

@@ -1,11 +1,12 @@
 """The projection plan (kb_kbest_plan, no device needed): every GPU parity
-case runs on the kernel and tile it was written for, and the workloads'
-plans are the ones the design describes."""
+case, its tile pinned as the GPU tests pin it, runs on the kernel and tile it
+was written for, and the workloads' plans (the cost models' own choices) are
+the ones the design describes."""
 import pytest
 
 import paper_1805_09863_amd as kb
 from paper_1805_09863_amd.binding import KBestError
-from tests.parity_cases import ARGMAX, FEW, SHARDS, SMALL, WIDE
+from tests.parity_cases import ARGMAX, FEW, SHARDS, SMALL, WIDE, tile_env
 
 
 def _code(dt: str) -> int:
@@ -17,38 +18,45 @@ def _plan_str(p: dict) -> str:
 
 
 @pytest.mark.parametrize("case", range(len(SMALL)))
-def test_small_case_plans(case):
+def test_small_case_plans(case, monkeypatch):
     rps, H, V, k, dt, want = SMALL[case]
+    tile_env(monkeypatch, want)
     assert _plan_str(kb.kbest_plan(_code(dt), sum(rps), H, V, k)) == want
 
 
 @pytest.mark.parametrize("case", range(len(WIDE)))
-def test_wide_case_plans(case):
+def test_wide_case_plans(case, monkeypatch):
     rps, H, V, k, want = WIDE[case]
+    tile_env(monkeypatch, want)
     assert _plan_str(kb.kbest_plan(kb.KB_BF16, sum(rps), H, V, k)) == want
 
 
 @pytest.mark.parametrize("case", range(len(FEW)))
-def test_few_case_plans(case):
+def test_few_case_plans(case, monkeypatch):
     rps, H, V, k, dt, want = FEW[case]
+    tile_env(monkeypatch, want)
     assert _plan_str(kb.kbest_plan(_code(dt), sum(rps), H, V, k)) == want
 
 
 @pytest.mark.parametrize("case", range(len(ARGMAX)))
-def test_argmax_case_plans(case):
+def test_argmax_case_plans(case, monkeypatch):
     N, H, V, dt, want = ARGMAX[case]
+    tile_env(monkeypatch, want)
     assert _plan_str(kb.kbest_plan(_code(dt), N, H, V, 1)) == want
 
 
 @pytest.mark.parametrize("case", range(len(SHARDS)))
-def test_shard_case_plans(case):
+def test_shard_case_plans(case, monkeypatch):
     rps, H, V, k, dt, cuts, want = SHARDS[case]
+    tile_env(monkeypatch, want)
     got = {_plan_str(kb.kbest_plan(_code(dt), sum(rps), H, b - a, k)) for a, b in zip(cuts, cuts[1:])}
     assert got == want
 
 
-def test_wide_cases_keep_their_edges():
+def test_wide_cases_keep_their_edges(monkeypatch):
     # the features the 256 x 256 cases are listed for
+    monkeypatch.setenv("KB_TILE", "256x256")
+
     def plan(i):
         rps, H, V, k, _ = WIDE[i]
         return kb.kbest_plan(kb.KB_BF16, sum(rps), H, V, k), sum(rps), V
@@ -69,7 +77,7 @@ def test_wide_cases_keep_their_edges():
 
 @pytest.mark.parametrize("dt,N,H,V,k,want", [
     ("f32", 5, 256, 8000, 5, ("few", 8, 64, 1, 125, 1)),              # one sentence, beam 5
-    ("f32", 320, 512, 30000, 5, ("dma", 32, 256, 10, 24, 5)),        # 64 sentences, beam 5
+    ("f32", 320, 512, 30000, 5, ("dma", 32, 128, 10, 47, 5)),        # 64 sentences, beam 5: two workgroups a CU
     ("bf16", 640, 1024, 60000, 5, ("wide", 256, 256, 3, 79, 3)),     # 128 sentences, beam 5
     ("bf16", 3072, 1024, 90000, 12, ("wide", 256, 256, 12, 21, 17)),  # 256 sentences, beam 12
     ("bf16", 2560, 1024, 50000, 5, ("wide", 256, 256, 10, 25, 8)),   # the decode loop's first step
@@ -99,7 +107,9 @@ def test_plan_split_invariants():
                 p = kb.kbest_plan(_code(dt), N, 256, V, 5)
                 nt = -(-V // p["tile_words"])
                 assert p["row_tiles"] == -(-N // p["tile_rows"])
-                assert 1 <= p["splits"] <= 256 and p["row_tiles"] * p["splits"] <= max(256, p["row_tiles"])
+                # one workgroup per CU, two of the DMA pipeline's 32 x 128 tile
+                per = 2 if (p["kernel"] == "dma" and p["tile_words"] == 128 and p["tile_rows"] == 32) else 1
+                assert 1 <= p["splits"] <= 256 and p["row_tiles"] * p["splits"] <= max(per * 256, p["row_tiles"])
                 assert (p["splits"] - 1) * p["tiles_per_split"] < nt <= p["splits"] * p["tiles_per_split"]
 
 

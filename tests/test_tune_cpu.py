@@ -30,7 +30,7 @@ def test_tile_override_follows_the_path(tile_env):
     assert _p(kb.KB_F32, 640, 1000, 60000) == "reg 32x512"
     tile_env("256x256")
     assert _p(kb.KB_BF16, 40, 1024, 50000) == "wide 256x256"
-    assert _p(kb.KB_F32, 320, 512, 30000) == "dma 32x256"             # no 256 x 256 tile there: ignored
+    assert _p(kb.KB_F32, 320, 512, 30000) == "dma 32x128"             # no 256 x 256 tile there: ignored
     assert _p(kb.KB_F32, 320, 520, 30000) == "reg 32x256"
     assert _p(kb.KB_BF16, 640, 1024, 60000, aligned=False) == "reg 256x128"
     assert _p(kb.KB_BF16, 300, 128, 200) == "dma 32x128"              # V < 256: ignored
@@ -69,8 +69,13 @@ def test_fit_recovers_the_model_and_evaluation_picks_it():
     assert ev["worst_ratio"] < 1.05 and ev["sum_us_model_choice"] <= 1.02 * ev["sum_us_best"]
 
 
-def test_workgroup_words_matches_the_plan():
-    for dt, N, H, V in ((kb.KB_F32, 320, 512, 30000), (kb.KB_BF16, 3072, 1024, 90000), (kb.KB_BF16, 100, 256, 8000)):
-        p = kb.kbest_plan(dt, N, H, V, 5)
-        assert tp.workgroup_words(N, V, p["tile_rows"], p["tile_words"]) == \
-            p["tile_rows"] * p["tile_words"] * p["tiles_per_split"]
+def test_workgroup_words_matches_the_plan(tile_env):
+    # the script's split rule, two 32 x 128 workgroups per CU on the DMA pipeline included
+    for dt, path, N, H, V in ((kb.KB_F32, "f32", 320, 512, 30000), (kb.KB_F32, "f32reg", 320, 520, 30000),
+                              (kb.KB_BF16, "bf16", 3072, 1024, 90000), (kb.KB_BF16, "bf16", 100, 256, 8000)):
+        for tile in (None, "32x128", "32x256", "128x256"):
+            tile_env(tile)
+            p = kb.kbest_plan(dt, N, H, V, 5)
+            t = f"{p['tile_rows']}x{p['tile_words']}"
+            assert tp.workgroup_words(N, V, p["tile_rows"], p["tile_words"], tp.per_cu(path, t)) == \
+                p["tile_rows"] * p["tile_words"] * p["tiles_per_split"]
