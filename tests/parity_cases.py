@@ -115,6 +115,8 @@ ARGMAX = [
     (790, 384, 6216, "bf16", "dma 256x128"),
     (65, 128, 44000, "bf16", "dma 128x256"),
     (33, 128, 17000, "bf16", "dma 32x512"),      # two row tiles
+    (300, 128, 9000, "f32", "dma 32x128"),       # float32 DMA pipeline, ten row tiles
+    (700, 64, 5004, "f32", "dma 256x128"),       # float32 DMA pipeline, ragged words
 ]
 
 # Vocabulary shards (Algorithm 6), each shard planned on its own words.
@@ -127,6 +129,7 @@ SHARDS = [
     ([16] * 3, 64, 4000, 16, "bf16", list(range(0, 4001, 500)), {"reg 128x256"}),  # 8 shards, k = 16
     ([1] * 37, 33, 1003, 3, "bf16", [0, 333, 1003], {"reg 128x256"}),           # unaligned H and V
     ([2, 7, 3], 128, 9000, 8, "bf16", [0, 8, 8992, 9000], {"dma 32x128"}),      # shards of 8 words beside a wide one
+    ([5] * 40, 128, 6000, 5, "f32", [0, 2996, 6000], {"dma 32x256"}),          # float32 DMA pipeline, ragged shards
 ]
 
 # Steps of at most 8 rows that the planner gives the few-row kernel (16-byte
