@@ -39,8 +39,8 @@
  *    the choice).  With the environment variable KB_TILE=<rows>x<words> at
  *    call time (e.g. 32x256) a step not taken by the few-row kernel uses that
  *    tile instead where its path has it: 128x256, 256x128, 32x512, 32x256
- *    or 32x128 on every path, and 256x256 on the bf16 DMA pipeline with
- *    V >= 256.  Other values are ignored.  It exists to measure the
+ *    or 32x128 on every path, 64x128 on the DMA pipeline, and 256x256 on the
+ *    bf16 DMA pipeline with V >= 256.  Other values are ignored.  It exists to measure the
  *    model (paper_1805_09863_amd/tune_planner.py); the workspace size follows
  *    it, so size the workspace with the same setting.
  *  - Size limits (KB_ERR_UNSUPPORTED beyond them): N * V <= INT_MAX (a

@@ -49,6 +49,7 @@ using LayL128 = Lay<4, 2, 2, 2>;  // 256 words x 128 rows
 using LayL32 = Lay<4, 1, 4, 1>;   // 512 words x 32 rows (few live rows)
 using LayL32M = Lay<2, 1, 4, 1>;  // 256 words x 32 rows (few rows, more vocabulary tiles)
 using LayL32S = Lay<1, 1, 4, 1>;  // 128 words x 32 rows (few rows, small vocabulary)
+using LayL64 = Lay<2, 1, 2, 2>;   // 128 words x 64 rows (DMA pipeline only, two workgroups per CU)
 
 template <class L>
 struct alignas(16) SmemEpi {

@@ -190,8 +190,14 @@ struct DmaKernel {
   }
 };
 
+// Waves per SIMD the compiler must leave registers for: two for the 64-row x
+// 128-word tile with k <= 8 (two workgroups per CU; the accumulators then sit
+// in the architectural registers, at most 256 per lane in all), else one.
+constexpr int dma_waves_per_eu(int bh, int bv, int kc) { return bh == 64 && bv == 128 && kc <= 8 ? 2 : 1; }
+
 template <class L, int KC, bool F32>
-__global__ __launch_bounds__(256) void k1_dma(K1Args a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(dma_waves_per_eu(L::BH, L::BV, KC))))
+void k1_dma(K1Args a) {
   using D = DmaKernel<L, KC, F32>;
   using G = DmaGeom<L, F32>;
   constexpr int BV = L::BV, BH = L::BH, WV = L::WV, WH = L::WH, NWV = L::NWV;

@@ -93,7 +93,7 @@ __device__ __forceinline__ void k1_cell(const K1Args& a, int b, int& row_tile, i
 }
 
 // Tile shapes of the fused projection kernel.
-enum K1Layout { K1_L256 = 0, K1_L128 = 1, K1_L32 = 2, K1_W256 = 3, K1_L32M = 4, K1_L32S = 5 };
+enum K1Layout { K1_L256 = 0, K1_L128 = 1, K1_L32 = 2, K1_W256 = 3, K1_L32M = 4, K1_L32S = 5, K1_L64 = 6 };
 
 // dma: the LDS-DMA pipeline (bf16, H % 128 == 0, V % 8 == 0, 16-byte aligned h and W);
 // layout K1_W256 (256 x 256 tiles) exists only with it.

@@ -35,6 +35,8 @@ hipError_t launch_k1_dma_f32_L128(int kc, dim3 grid, const K1Args& a, hipStream_
 hipError_t launch_k1_dma_f32_L32(int kc, dim3 grid, const K1Args& a, hipStream_t st);
 hipError_t launch_k1_dma_f32_L32M(int kc, dim3 grid, const K1Args& a, hipStream_t st);
 hipError_t launch_k1_dma_f32_L32S(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_dma_L64(int kc, dim3 grid, const K1Args& a, hipStream_t st);
+hipError_t launch_k1_dma_f32_L64(int kc, dim3 grid, const K1Args& a, hipStream_t st);
 
 hipError_t launch_k1(int bf16, int dma, int layout, int kc, dim3 grid, const K1Args& a, hipStream_t st) {
   if (dma && !bf16) {
@@ -44,6 +46,7 @@ hipError_t launch_k1(int bf16, int dma, int layout, int kc, dim3 grid, const K1A
       case K1_L32M: return launch_k1_dma_f32_L32M(kc, grid, a, st);
       case K1_L32S: return launch_k1_dma_f32_L32S(kc, grid, a, st);
       case K1_L32: return launch_k1_dma_f32_L32(kc, grid, a, st);
+      case K1_L64: return launch_k1_dma_f32_L64(kc, grid, a, st);
       default: return hipErrorInvalidValue;  // the 256 x 256 tile is bf16 only
     }
   }
@@ -54,6 +57,7 @@ hipError_t launch_k1(int bf16, int dma, int layout, int kc, dim3 grid, const K1A
       case K1_L128: return launch_k1_dma_L128(kc, grid, a, st);
       case K1_L32M: return launch_k1_dma_L32M(kc, grid, a, st);
       case K1_L32S: return launch_k1_dma_L32S(kc, grid, a, st);
+      case K1_L64: return launch_k1_dma_L64(kc, grid, a, st);
       default: return launch_k1_dma_L32(kc, grid, a, st);
     }
   }
@@ -133,8 +137,9 @@ constexpr size_t kFewLdsMax = 160 * 1024;
 constexpr long long kFewMaxWorkF32 = 1ll << 30;
 
 // Tile choice by a cost model.  A step's projection takes about
-//   (a H + e) x (rows x words one workgroup covers) + f  microseconds,
-// the workgroup covering row tile x word tile x tiles per split.  a, e and f
+//   (a H + e) x (rows x words one workgroup covers) x slots + f  microseconds,
+// the workgroup covering row tile x word tile x tiles per split, slots = 2
+// for a tile planned at two workgroups per CU whose grid exceeds one per CU.  a, e and f
 // per layout are fitted by tune_planner.py to the projection times of every
 // layout forced in turn (KB_TILE; k = 5) over 40-1280 rows (bf16 2560), one
 // table per path: float32 register-staged and float32 on the DMA pipeline at
@@ -155,27 +160,37 @@ constexpr TileCost kF32Costs[] = {
     {kb::K1_L32S, 32, 128, 7.6774e-06, 8.7361e-04, 18.167},
 };
 constexpr TileCost kBf16DmaCosts[] = {
-    {kb::K1_W256, 256, 256, 3.1793e-07, 2.2198e-04, 15.664},
-    {kb::K1_L128, 128, 256, 5.0300e-07, 3.4708e-04, 19.122},
-    {kb::K1_L256, 256, 128, 4.8212e-07, 3.4390e-04, 17.873},
-    {kb::K1_L32, 32, 512, 9.7784e-07, 3.7621e-04, 17.473},
-    {kb::K1_L32M, 32, 256, 1.2656e-06, 5.0371e-04, 20.632},
-    {kb::K1_L32S, 32, 128, 2.7966e-06, 7.1836e-04, 15.656},
+    {kb::K1_W256, 256, 256, 3.1048e-07, 2.2403e-04, 15.484},
+    {kb::K1_L128, 128, 256, 4.9823e-07, 3.4975e-04, 18.980},
+    {kb::K1_L256, 256, 128, 4.8626e-07, 3.4485e-04, 17.401},
+    {kb::K1_L32, 32, 512, 9.8166e-07, 3.7969e-04, 17.161},
+    {kb::K1_L32M, 32, 256, 1.2685e-06, 5.1027e-04, 20.342},
+    {kb::K1_L32S, 32, 128, 1.4177e-06, 3.1844e-04, 18.122},
+    {kb::K1_L64, 64, 128, 7.7745e-07, 2.1370e-04, 17.918},
 };
 // float32 on the DMA pipeline (fp32 MFMA, operands straight from LDS)
 constexpr TileCost kF32DmaCosts[] = {
-    {kb::K1_L128, 128, 256, 3.6700e-06, 4.2906e-04, 15.920},
-    {kb::K1_L256, 256, 128, 3.6914e-06, 4.2281e-04, 14.781},
-    {kb::K1_L32, 32, 512, 4.4750e-06, 5.0180e-04, 15.731},
-    {kb::K1_L32M, 32, 256, 4.9317e-06, 6.5060e-04, 19.367},
-    {kb::K1_L32S, 32, 128, 8.7460e-06, 1.6116e-03, 12.312},
+    {kb::K1_L128, 128, 256, 3.6907e-06, 4.3125e-04, 15.592},
+    {kb::K1_L256, 256, 128, 3.7159e-06, 4.2437e-04, 14.462},
+    {kb::K1_L32, 32, 512, 4.4843e-06, 5.1425e-04, 15.031},
+    {kb::K1_L32M, 32, 256, 4.9426e-06, 6.6724e-04, 18.698},
+    {kb::K1_L32S, 32, 128, 4.6148e-06, 5.8893e-04, 18.438},
+    {kb::K1_L64, 64, 128, 4.1449e-06, 2.7480e-04, 17.195},
 };
 
-// Workgroups of a layout that one CU holds at once.  The DMA pipeline's
-// 32 x 128 tile takes 60 KB of LDS and at most 220 registers per lane, so two
-// run side by side and one's epilogue and barrier waits overlap the other's
-// products (its grid may reach 512 workgroups); every other tile fills a CU.
-int per_cu(int layout, bool dma) { return dma && layout == kb::K1_L32S ? 2 : 1; }
+// k rounded up to the k-list lengths the projection kernels are built for
+int kc_of(int k) { return k <= 4 ? 4 : (k <= 8 ? 8 : (k <= 12 ? 12 : 16)); }
+
+// Workgroups of a layout that one CU holds at once.  On the DMA pipeline the
+// 32 x 128 tile (60 KB of LDS, at most 220 registers per lane) and, with
+// k <= 8, the 64 x 128 tile (67 KB, built for at most 256 registers) run two
+// side by side, one's epilogue and barrier waits overlapping the other's
+// products (their grids may reach 512 workgroups); every other tile, and the
+// 64 x 128 one with longer lists, fills a CU.
+int per_cu(int layout, bool dma, int kc) {
+  if (!dma) return 1;
+  return layout == kb::K1_L32S || (layout == kb::K1_L64 && kc <= 8) ? 2 : 1;
+}
 
 // splits of the vocabulary for a layout: per_cu workgroups per CU over the row tiles
 int splits_for(int row_tiles, int n_vtiles, int per) {
@@ -188,13 +203,18 @@ int splits_for(int row_tiles, int n_vtiles, int per) {
 
 // the layout of the least modelled time among n (ties keep the earlier)
 template <size_t n>
-void pick_by_model(const TileCost (&costs)[n], int N, int H, int V, bool dma, Plan& p) {
+void pick_by_model(const TileCost (&costs)[n], int N, int H, int V, bool dma, int kc, Plan& p) {
   double best = -1.0;
   for (const TileCost& c : costs) {
     if (c.layout == kb::K1_W256 && V < kWideMinCols) continue;
+    if (c.layout == kb::K1_L64 && kc > 8) continue;  // fitted at two workgroups per CU
     const int rt = (N + c.BH - 1) / c.BH, nt = (V + c.BV - 1) / c.BV;
-    const int P = splits_for(rt, nt, per_cu(c.layout, dma)), tps = (nt + P - 1) / P;
-    const double t = (c.a * H + c.e) * (double)c.BH * c.BV * tps + c.f;
+    const int per = per_cu(c.layout, dma, kc);
+    const int P = splits_for(rt, nt, per), tps = (nt + P - 1) / P;
+    // a CU that holds two workgroups runs both: twice the words at the
+    // co-resident rate (the fit's), once the grid exceeds one per CU
+    const int slots = per == 2 && rt * ((nt + tps - 1) / tps) > kTargetCUs ? 2 : 1;
+    const double t = (c.a * H + c.e) * (double)c.BH * c.BV * tps * slots + c.f;
     if (best < 0.0 || t < best) {
       best = t;
       p.layout = c.layout;
@@ -209,9 +229,9 @@ constexpr long long kFewMaxWeightsBf16 = 64ll << 20;
 // KB_TILE=<rows>x<words> (e.g. 32x256) at call time replaces the modelled
 // choice by that tile where the step's path has it (for measuring the cost
 // model; the tuning script sets it): 128x256, 256x128, 32x512, 32x256,
-// 32x128, and 256x256 on the bf16 DMA pipeline with V >= 256 (wide_ok).
-// Other values are ignored.
-void apply_tile_override(bool wide_ok, Plan& p) {
+// 32x128, 64x128 on the DMA pipeline (dma), and 256x256 on the bf16 DMA
+// pipeline with V >= 256 (wide_ok).  Other values are ignored.
+void apply_tile_override(bool dma, bool wide_ok, Plan& p) {
   const char* e = getenv("KB_TILE");
   int r = 0, w = 0;
   char tail = 0;
@@ -223,6 +243,7 @@ void apply_tile_override(bool wide_ok, Plan& p) {
   else if (r == 32 && w == 512) layout = kb::K1_L32;
   else if (r == 32 && w == 256) layout = kb::K1_L32M;
   else if (r == 32 && w == 128) layout = kb::K1_L32S;
+  else if (r == 64 && w == 128 && dma) layout = kb::K1_L64;
   if (layout < 0) return;
   p.layout = layout;
   p.BH = r;
@@ -245,11 +266,11 @@ Plan make_plan(int dtype, int N, int H, int V, int k, bool dma, bool vec) {
     p.BV = few_cw;
   } else if (dma && dma_shape(dtype, H, V)) {
     if (dtype == KB_BF16)
-      pick_by_model(kBf16DmaCosts, N, H, V, true, p);
+      pick_by_model(kBf16DmaCosts, N, H, V, true, kc_of(k), p);
     else
-      pick_by_model(kF32DmaCosts, N, H, V, true, p);
+      pick_by_model(kF32DmaCosts, N, H, V, true, kc_of(k), p);
   } else if (dtype == KB_F32) {
-    pick_by_model(kF32Costs, N, H, V, false, p);
+    pick_by_model(kF32Costs, N, H, V, false, kc_of(k), p);
   } else if (N > 192 && dtype == KB_BF16) {
     p.layout = kb::K1_L256;
     p.BH = 256;
@@ -279,12 +300,12 @@ Plan make_plan(int dtype, int N, int H, int V, int k, bool dma, bool vec) {
     }
     p.BH = 32;
   }
-  if (p.layout != kb::K1_FEW)
-    apply_tile_override(dtype == KB_BF16 && dma && dma_shape(dtype, H, V) && V >= kWideMinCols, p);
-  p.kc = k <= 4 ? 4 : (k <= 8 ? 8 : (k <= 12 ? 12 : 16));
+  const bool dma_path = dma && dma_shape(dtype, H, V);
+  if (p.layout != kb::K1_FEW) apply_tile_override(dma_path, dtype == KB_BF16 && dma_path && V >= kWideMinCols, p);
+  p.kc = kc_of(k);
   p.row_tiles = (N + p.BH - 1) / p.BH;
   p.n_vtiles = (V + p.BV - 1) / p.BV;
-  const int P = splits_for(p.row_tiles, p.n_vtiles, per_cu(p.layout, dma && dma_shape(dtype, H, V)));
+  const int P = splits_for(p.row_tiles, p.n_vtiles, per_cu(p.layout, dma_path, p.kc));
   p.tps = (p.n_vtiles + P - 1) / P;
   p.P = (p.n_vtiles + p.tps - 1) / p.tps;  // no empty split
   p.stats_off = 0;

@@ -6,7 +6,9 @@ projection kernel of kbest_step is timed with HIP events on its own stream
 (median of the timed launches after warm-up).  Then, per tile, the model
 
     t = (a H + e) w + f        w = rows x words one workgroup covers
-                                 = tile rows x tile words x tiles per split
+                                 = tile rows x tile words x tiles per split,
+                                 doubled for a tile at two workgroups per CU
+                                 whose grid exceeds 256 workgroups
 
 is fitted by least squares on relative error, and the choice the model
 makes on each shape is compared with the fastest tile measured there.  The
@@ -38,12 +40,12 @@ from paper_1805_09863_amd.hipevents import HipEvents
 
 TILES = {  # KB_TILE value -> (rows, words) per tile
     "256x256": (256, 256), "128x256": (128, 256), "256x128": (256, 128),
-    "32x512": (32, 512), "32x256": (32, 256), "32x128": (32, 128),
+    "32x512": (32, 512), "32x256": (32, 256), "32x128": (32, 128), "64x128": (64, 128),
 }
 GRIDS = {
     "f32": dict(H=(256, 512, 1024, 2048), V=(8000, 30000, 60000),
                 N=(40, 64, 100, 160, 240, 320, 480, 640, 960, 1280),
-                tiles=("128x256", "256x128", "32x512", "32x256", "32x128")),
+                tiles=("128x256", "256x128", "32x512", "32x256", "32x128", "64x128")),
     "f32reg": dict(H=(264, 520, 1032, 2056), V=(8000, 30000, 60000),
                    N=(40, 64, 100, 160, 240, 320, 480, 640, 960, 1280),
                    tiles=("128x256", "256x128", "32x512", "32x256", "32x128")),
@@ -54,9 +56,9 @@ GRIDS = {
 
 
 def per_cu(dtype, tile: str) -> int:
-    """Workgroups one CU holds at once, as the planner counts them: two of the
-    DMA pipeline's 32 x 128 tile, one of every other."""
-    return 2 if dtype in ("f32", "bf16") and tile == "32x128" else 1
+    """Workgroups one CU holds at once, as the planner counts them at k <= 8:
+    two of the DMA pipeline's 32 x 128 and 64 x 128 tiles, one of every other."""
+    return 2 if dtype in ("f32", "bf16") and tile in ("32x128", "64x128") else 1
 
 
 def workgroup_words(N: int, V: int, rows: int, words: int, per: int = 1) -> int:
@@ -64,6 +66,15 @@ def workgroup_words(N: int, V: int, rows: int, words: int, per: int = 1) -> int:
     rt, nt = -(-N // rows), -(-V // words)
     P = max(1, min(per * 256 // rt, nt, 256))
     return rows * words * -(-nt // P)
+
+
+def model_words(N: int, V: int, rows: int, words: int, per: int = 1) -> int:
+    """The model's w: a workgroup's rows x words, doubled for a tile planned at
+    two workgroups per CU once its grid (row tiles x splits) exceeds 256."""
+    w = workgroup_words(N, V, rows, words, per)
+    rt, nt = -(-N // rows), -(-V // words)
+    tps = w // (rows * words)
+    return w * (2 if per == 2 and rt * -(-nt // tps) > 256 else 1)
 
 
 def measure(dtype: str, grid: dict, reps: int, log) -> list:
@@ -121,7 +132,7 @@ def fit(rows: list, tiles, dtype=None) -> dict:
         if len(pts) < 3:
             continue
         pc = per_cu(dtype, tile)
-        X = np.array([[x["H"] * workgroup_words(x["N"], x["V"], r, w, pc), workgroup_words(x["N"], x["V"], r, w, pc), 1.0]
+        X = np.array([[x["H"] * model_words(x["N"], x["V"], r, w, pc), model_words(x["N"], x["V"], r, w, pc), 1.0]
                       for x in pts])
         y = np.array([x["us"][tile] for x in pts])
         c, *_ = np.linalg.lstsq(X / y[:, None], np.ones_like(y), rcond=None)
@@ -141,7 +152,7 @@ def evaluate(rows: list, model: dict, dtype=None) -> dict:
 
         def pred(t):
             r, w = TILES[t]
-            wg = workgroup_words(x["N"], x["V"], r, w, per_cu(dtype, t))
+            wg = model_words(x["N"], x["V"], r, w, per_cu(dtype, t))
             m = model[t]
             return (m["a"] * x["H"] + m["e"]) * wg + m["f"]
         choice = min(cands, key=pred)

@@ -75,6 +75,11 @@ SMALL = [
     ([5] * 78, 96, 5004, 5, "f32", "reg 32x512"),            # 13 row tiles
     ([20, 20], 96, 1004, 4, "f32", "reg 32x128"),            # two row tiles
     ([23] * 7, 64, 65001, 12, "f32", "reg 128x256"),           # V odd: scalar loads
+    # the DMA pipeline's 64 x 128 tile: two workgroups per CU at k <= 8, one above
+    ([5] * 61, 128, 5000, 5, "bf16", "dma 64x128"),          # 305 rows: 5 row tiles, the last ragged
+    ([12] * 11, 256, 9000, 12, "bf16", "dma 64x128"),        # k = 12
+    ([3] * 43, 64, 33004, 3, "f32", "dma 64x128"),           # 2 tiles per split
+    ([16] * 9, 128, 7004, 16, "f32", "dma 64x128"),          # k = 16, words 7004 = 54 x 128 + 92
 ]
 
 # The 256 x 256-tile projection kernel (bf16, H % 128 == 0, V % 8 == 0, and

@@ -10,9 +10,9 @@ from tests.gpu_util import check, run_step, say
 
 pytestmark = pytest.mark.gpu
 
-DMA_TILES = ("256x256", "128x256", "256x128", "32x512", "32x256", "32x128")
+DMA_TILES = ("256x256", "128x256", "256x128", "32x512", "32x256", "32x128", "64x128")
 REG_TILES = ("128x256", "256x128", "32x512", "32x256", "32x128")
-F32_DMA_TILES = REG_TILES                           # the 256 x 256 tile is bf16 only
+F32_DMA_TILES = REG_TILES + ("64x128",)            # the 256 x 256 tile is bf16 only
 STEPS = [
     # (rows per sentence, H, V, k, dtype, tiles): bf16 DMA pipeline, register-staged, float32 DMA
     ([7] * 43, 128, 5000, 7, "bf16", DMA_TILES),     # 301 rows, ragged words (5000 = 19 x 256 + 136)

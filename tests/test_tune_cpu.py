@@ -30,10 +30,14 @@ def test_tile_override_follows_the_path(tile_env):
     assert _p(kb.KB_F32, 640, 1000, 60000) == "reg 32x512"
     tile_env("256x256")
     assert _p(kb.KB_BF16, 40, 1024, 50000) == "wide 256x256"
-    assert _p(kb.KB_F32, 320, 512, 30000) == "dma 32x128"             # no 256 x 256 tile there: ignored
+    assert _p(kb.KB_F32, 320, 512, 30000) == "dma 64x128"             # no 256 x 256 tile there: ignored
     assert _p(kb.KB_F32, 320, 520, 30000) == "reg 32x256"
     assert _p(kb.KB_BF16, 640, 1024, 60000, aligned=False) == "reg 256x128"
     assert _p(kb.KB_BF16, 300, 128, 200) == "dma 32x128"              # V < 256: ignored
+    tile_env("64x128")
+    assert _p(kb.KB_BF16, 640, 1024, 60000) == "dma 64x128"
+    assert _p(kb.KB_F32, 640, 1024, 60000) == "dma 64x128"
+    assert _p(kb.KB_BF16, 640, 1000, 60000) == "reg 256x128"            # the register-staged path has no 64-row tile: ignored
     tile_env("128x256")
     assert _p(kb.KB_F32, 5, 256, 8000) == "few 8x64"                  # the few-row kernel keeps its steps
     for bad in ("64x64", "32x256x", "x", "", "256"):
