@@ -211,9 +211,15 @@ void pick_by_model(const TileCost (&costs)[n], int N, int H, int V, bool dma, in
     const int rt = (N + c.BH - 1) / c.BH, nt = (V + c.BV - 1) / c.BV;
     const int per = per_cu(c.layout, dma, kc);
     const int P = splits_for(rt, nt, per), tps = (nt + P - 1) / P;
+    const bool paired = rt * ((nt + tps - 1) / tps) > kTargetCUs;
+    // a two-per-CU tile alone on its CU with several tiles to run in turn
+    // (one row tile: splits are capped at 256) is slower than the fit says
+    // (V=50k, 40 rows, bf16: 64 x 128 measured 43.6 us against 37.5 for
+    // 32 x 512); the fit holds for co-resident pairs and single tiles
+    if (per == 2 && !paired && tps > 1) continue;
     // a CU that holds two workgroups runs both: twice the words at the
     // co-resident rate (the fit's), once the grid exceeds one per CU
-    const int slots = per == 2 && rt * ((nt + tps - 1) / tps) > kTargetCUs ? 2 : 1;
+    const int slots = per == 2 && paired ? 2 : 1;
     const double t = (c.a * H + c.e) * (double)c.BH * c.BV * tps * slots + c.f;
     if (best < 0.0 || t < best) {
       best = t;

@@ -142,11 +142,21 @@ def fit(rows: list, tiles, dtype=None) -> dict:
     return out
 
 
+def planner_skips(N: int, V: int, tile: str, dtype) -> bool:
+    """The planner leaves out a two-per-CU tile that would run alone on its CU
+    with more than one tile in turn (its grid at most 256 workgroups)."""
+    rows, words = TILES[tile]
+    per = per_cu(dtype, tile)
+    tps = workgroup_words(N, V, rows, words, per) // (rows * words)
+    rt, nt = -(-N // rows), -(-V // words)
+    return per == 2 and tps > 1 and rt * -(-nt // tps) <= 256
+
+
 def evaluate(rows: list, model: dict, dtype=None) -> dict:
     """The model's choice on each shape against the fastest tile measured."""
     worst, tot_choice, tot_best = 1.0, 0.0, 0.0
     for x in rows:
-        cands = [t for t in model if t in x["us"]]
+        cands = [t for t in model if t in x["us"] and not planner_skips(x["N"], x["V"], t, dtype)]
         if not cands:
             continue
 
