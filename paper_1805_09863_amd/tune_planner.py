@@ -178,12 +178,30 @@ def main():
     ap.add_argument("--dtype", choices=tuple(GRIDS), required=True)
     ap.add_argument("--reps", type=int, default=15)
     ap.add_argument("--out", required=True, help="JSON: measured times, fitted constants, evaluation")
+    ap.add_argument("--rows", help="comma-separated row counts in place of the grid's (e.g. 9,16,24,32)")
+    ap.add_argument("--check", action="store_true",
+                    help="no fit: compare the library's own choice (kb_kbest_plan) with the fastest tile")
     args = ap.parse_args()
 
     def log(msg):
         print(msg, file=sys.stderr, flush=True)
-    grid = GRIDS[args.dtype]
+    grid = dict(GRIDS[args.dtype])
+    if args.rows:
+        grid["N"] = tuple(int(x) for x in args.rows.split(","))
     rows = measure(args.dtype, grid, args.reps, log)
+    if args.check:
+        code = binding.KB_BF16 if args.dtype == "bf16" else binding.KB_F32
+        for x in rows:
+            p = binding.kbest_plan(code, x["N"], x["H"], x["V"], 5)
+            x["planner"] = f"{p['tile_rows']}x{p['tile_words']}"
+        res = {"dtype": args.dtype, "grid": {k: list(v) for k, v in grid.items()}, "rows": rows,
+               "sum_us_planner": sum(x["us"][x["planner"]] for x in rows),
+               "sum_us_best": sum(min(x["us"].values()) for x in rows),
+               "worst_ratio": max(x["us"][x["planner"]] / min(x["us"].values()) for x in rows)}
+        with open(args.out, "w") as f:
+            json.dump(res, f)
+        log(json.dumps({k: v for k, v in res.items() if k.startswith(("sum", "worst"))}))
+        return
     model = fit(rows, grid["tiles"], args.dtype)
     # the register-staged float32 planner leaves out the 256-row tile (it fits the model poorly)
     used = {t: m for t, m in model.items() if not (args.dtype == "f32reg" and t == "256x128")}
