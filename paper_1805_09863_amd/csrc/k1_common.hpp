@@ -143,12 +143,12 @@ struct Epilogue {
 #pragma unroll
     for (int hb = 0; hb < WH; ++hb) {
       const int row = min(h0 + (wh * WH + hb) * 32 + col, a.N - 1);
-      tg[hb] = __hip_atomic_load(&a.gthr[row], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      tg[hb] = a.share ? __hip_atomic_load(&a.gthr[row], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
     }
   }
 
   __device__ __forceinline__ void owner_publish(const K1Args& a, int row, float v) {
-    if (row < a.N && v > published) {
+    if (a.share && row < a.N && v > published) {
       atomicMax(&a.gthr[row], f2key(v));
       published = v;
     }

@@ -117,7 +117,7 @@ struct DmaKernel {
         const int v = min(v0 + (wave * B_PER_WAVE + lane) * 4, a.V - 4);  // words >= V are masked
         dma16(a.b + v, bias_lds + wave * B_PER_WAVE * 16);
       }
-      if (lane < T_PER_WAVE) dma16(a.gthr + o.trow, tgk_lds + wave * T_PER_WAVE * 16);
+      if (a.share && lane < T_PER_WAVE) dma16(a.gthr + o.trow, tgk_lds + wave * T_PER_WAVE * 16);
     }
   }
 
@@ -286,7 +286,7 @@ void k1_dma(K1Args a) {
     {
       const int wh = wave / NWV, col = lane & 31;
 #pragma unroll
-      for (int hb = 0; hb < WH; ++hb) tg[hb] = ep.tgk[par][(wh * WH + hb) * 32 + col];
+      for (int hb = 0; hb < WH; ++hb) tg[hb] = a.share ? ep.tgk[par][(wh * WH + hb) * 32 + col] : 0u;
     }
     epi.tile(acc, ep, a, h0, vt * BV, vt == vt0, tg, ep.bias[par]);
   }

@@ -68,6 +68,9 @@ struct K1Args {
   int grp;            // row tiles per XCD group
   int no_stats;       // 1: the statistics may be skipped (greedy argmax; only the
                       //    256 x 256 tile kernel, k = 1, uses it)
+  int share;          // 1: rows' thresholds are shared through gthr; 0: gthr is neither
+                      //    read nor written (the other tiles' kernels; the 256 x 256 one
+                      //    always shares)
   float* logits;      // N x V scores p = W h (the unfused baseline's projection only)
 };
 

@@ -423,8 +423,13 @@ kb_status launch_projection(int dtype, int N, int H, int V, int k, const void* h
   a1.grp = p.row_tiles < 4 ? p.row_tiles : 4;
   a1.no_stats = (no_stats && p.layout == kb::K1_W256 && p.kc == 4) ? 1 : 0;
 
+  // With one tile per split and every workgroup resident from the start, no
+  // workgroup reads a threshold before the others publish theirs: the other
+  // tiles' kernels then share none, and the reset is not needed.
+  const bool all_resident = p.P * p.row_tiles <= per_cu(p.layout, dma, p.kc) * kTargetCUs;
+  a1.share = (p.layout == kb::K1_W256 || p.tps > 1 || !all_resident) ? 1 : 0;
   hipError_t e = hipSuccess;
-  if (p.layout != kb::K1_FEW) {  // the few-row kernel shares no thresholds
+  if (p.layout != kb::K1_FEW && a1.share) {  // the few-row kernel shares no thresholds
     const int n_zero = p.row_tiles * p.BH * (p.layout == kb::K1_W256 ? 1 + kGmaxSplits : 1);  // gthr (+ gmax)
     e = kb::launch_zero_u32(a1.gthr, n_zero, hs);
     if (e != hipSuccess) return fail(KB_ERR_HIP, "threshold reset kernel launch: %s", hipGetErrorString(e));
